@@ -1,0 +1,362 @@
+"""Plain fp64 CPU oracle for SIFT's bitmap-driven sparse prefill attention.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import or call this
+module; only the tests, the smoke check and the benchmark's CPU-baseline leg do.
+It shares no code with the HIP library: it reads the packed bit vectors with its
+own bit reader, builds the token-level mask from the definition, and runs a
+textbook masked softmax attention in float64 with numpy.
+
+What the oracle computes (paper: SIFT, arXiv 2606.09441):
+
+* A prompt is a list of RAG documents followed by the user query
+  (Section 3.1, decomposition of the attention matrix).  Tokens of different
+  prompts never see each other.
+* Attention is causal.  Rows of the user query attend to every earlier token
+  of their prompt (Section 3.1: the query sub-matrix is always recomputed;
+  Section 5.1: query M-blocks count every causal N-block).
+* Inside a document, key tile j of query-row tile i (j < i) is visible iff bit
+  i(i+1)/2 + j of the document's local-attention (LA) vector is set
+  (Section 4.1: T x T tiles of the lower triangle, enumerated row-major
+  (0,0),(1,0),(1,1),(2,0),..., packed most-significant-bit first, each
+  document's vector byte aligned).  Diagonal tiles (j == i) are always
+  computed, whatever their stored bit says.
+* Key page p of an earlier document e is visible to every row of a later
+  document of the same prompt iff bit p of e's cross-attention (CA) vector is
+  set (Section 4.2: one bit per KV page of width T, set = recomputed for future
+  documents; Section 3.4: selection by whole key column).
+* Sizes (Section 4.3): P = ceil(L/T) pages; LA = ceil(P(P+1)/16) bytes,
+  CA = ceil(P/8) bytes, per (layer, head, document).
+* Skipped tiles take part in neither numerator nor denominator: the result is
+  the softmax over the marked locations only (Section 5.2: only the iteration
+  over N-blocks changes; softmax and epilogue are those of dense attention).
+* The decoded list of a (head, M-block) holds every N-block the mask touches,
+  in ascending order (Section 5.1, sparse_n_indices).
+
+Readings where the paper is silent (each one is listed in DESIGN.md): "head"
+means query head; the kv head of query head h is h // (Hq / Hkv); tiles are
+segment local (a tile never straddles a document or the query, and the last
+tile of a segment may be partial); CA bits are MSB first by page index; the
+softmax scale is 1/sqrt(D); the bit-vector buffers concatenate, over prompts,
+documents in prompt order and query heads 0..Hq-1, each document's vector; the
+global number of tile i of segment s is the number of tiles in all earlier
+segments (of all prompts) plus i.
+
+All inputs are taken at their exact values: bf16 or fp32 numbers are widened
+to float64 without rounding.
+"""
+
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+# ----------------------------------------------------------------------------
+# Bit-vector format (Sections 4.1-4.3)
+# ----------------------------------------------------------------------------
+
+
+def num_pages(length: int, tile: int) -> int:
+    """P = ceil(L / T) (Section 4.3)."""
+    return -(-int(length) // int(tile))
+
+
+def la_num_bits(P: int) -> int:
+    """Tiles in a P x P lower triangle, diagonal included (Section 4.1)."""
+    return P * (P + 1) // 2
+
+
+def ca_num_bits(P: int) -> int:
+    """One bit per KV page (Section 4.2)."""
+    return P
+
+
+def la_num_bytes(P: int) -> int:
+    """ceil(P(P+1) / (2*8)) bytes (Section 4.3)."""
+    return -(-(P * (P + 1)) // 16)
+
+
+def ca_num_bytes(P: int) -> int:
+    """ceil(P / 8) bytes (Section 4.3)."""
+    return -(-P // 8)
+
+
+def la_bit_position(i: int, j: int) -> int:
+    """Position of tile (row i, column j), j <= i, in the row-major lower
+    triangle enumeration (0,0),(1,0),(1,1),(2,0),... (Section 4.1)."""
+    assert 0 <= j <= i
+    return i * (i + 1) // 2 + j
+
+
+def read_bit(buf, byte_offset: int, b: int) -> int:
+    """Bit b of the vector starting at byte_offset; the most significant bit
+    of each byte comes first (Section 4.1)."""
+    byte = int(buf[byte_offset + (b >> 3)])
+    return (byte >> (7 - (b & 7))) & 1
+
+
+# ----------------------------------------------------------------------------
+# Prompt layout
+# ----------------------------------------------------------------------------
+
+
+@dataclass
+class Segment:
+    prompt: int
+    is_query: bool
+    start: int          # first token on the packed token axis
+    length: int
+    pages: int          # P = ceil(length / T)
+    tile_base: int      # global number of the segment's tile 0
+    la_offset: int      # byte offset of the LA vector of query head 0 (documents)
+    ca_offset: int      # byte offset of the CA vector of query head 0 (documents)
+
+
+class Layout:
+    """Prompt b owns segments prompt_seg_ptr[b] .. prompt_seg_ptr[b+1]-1; the
+    last of them is the user query, the others are its documents in order.
+    Segment s covers tokens seg_offsets[s] .. seg_offsets[s+1]-1."""
+
+    def __init__(self, seg_offsets, prompt_seg_ptr, tile: int, num_q_heads: int):
+        self.seg_offsets = [int(x) for x in seg_offsets]
+        self.prompt_seg_ptr = [int(x) for x in prompt_seg_ptr]
+        self.tile = int(tile)
+        self.hq = int(num_q_heads)
+        self.segs: list[Segment] = []
+        tile_base = la_off = ca_off = 0
+        for b in range(len(self.prompt_seg_ptr) - 1):
+            first, last = self.prompt_seg_ptr[b], self.prompt_seg_ptr[b + 1] - 1
+            for s in range(first, last + 1):
+                start = self.seg_offsets[s]
+                length = self.seg_offsets[s + 1] - start
+                P = num_pages(length, self.tile)
+                self.segs.append(Segment(b, s == last, start, length, P,
+                                         tile_base, la_off, ca_off))
+                if s != last:
+                    la_off += self.hq * la_num_bytes(P)
+                    ca_off += self.hq * ca_num_bytes(P)
+                tile_base += P
+        self.num_tiles = tile_base
+        self.la_bytes = la_off
+        self.ca_bytes = ca_off
+        self.num_prompts = len(self.prompt_seg_ptr) - 1
+        self.num_tokens = self.seg_offsets[-1]
+
+    def prompt_segs(self, b: int) -> list[Segment]:
+        return [s for s in self.segs if s.prompt == b]
+
+    def prompt_span(self, b: int) -> tuple[int, int]:
+        ps = self.prompt_segs(b)
+        return ps[0].start, ps[-1].start + ps[-1].length
+
+    def tile_span(self, m: int) -> tuple[Segment, int, int, int]:
+        """(segment, local tile i, first token, token count) of global tile m."""
+        for s in self.segs:
+            if s.tile_base <= m < s.tile_base + s.pages:
+                i = m - s.tile_base
+                a = s.start + i * self.tile
+                return s, i, a, min(self.tile, s.start + s.length - a)
+        raise IndexError(m)
+
+
+# ----------------------------------------------------------------------------
+# The mask (Sections 3.1, 4.1, 4.2)
+# ----------------------------------------------------------------------------
+
+
+def _tile_row(lay: Layout, la, ca, head: int, b: int, seg_index: int, i: int) -> np.ndarray:
+    """Key visibility for every row of tile i of segment seg_index (prompt b),
+    before the causal cut: one bool per token of the prompt."""
+    ps = lay.prompt_segs(b)
+    p0, p1 = lay.prompt_span(b)
+    row = np.zeros(p1 - p0, dtype=bool)
+    me = ps[seg_index]
+    for si, se in enumerate(ps):
+        a = se.start - p0
+        if me.is_query:
+            # the user query recomputes everything before it (Section 3.1)
+            row[a:a + se.length] = True
+        elif si < seg_index:
+            # cross attention: page p of an earlier document (Section 4.2)
+            off = se.ca_offset + head * ca_num_bytes(se.pages)
+            for page in range(se.pages):
+                lo, hi = page * lay.tile, min((page + 1) * lay.tile, se.length)
+                row[a + lo:a + hi] = bool(read_bit(ca, off, page))
+        elif si == seg_index:
+            # local attention: tiles j <= i of the same document (Section 4.1)
+            off = se.la_offset + head * la_num_bytes(se.pages)
+            for j in range(i + 1):
+                bit = 1 if j == i else read_bit(la, off, la_bit_position(i, j))
+                lo, hi = j * lay.tile, min((j + 1) * lay.tile, se.length)
+                row[a + lo:a + hi] = bool(bit)
+    return row
+
+
+def mask_rows(lay: Layout, la, ca, head: int, b: int, rows) -> np.ndarray:
+    """allowed[r, k] for the prompt-relative query tokens `rows` of prompt b
+    against every key token of that prompt, for query head `head`."""
+    ps = lay.prompt_segs(b)
+    p0, p1 = lay.prompt_span(b)
+    keys = np.arange(p1 - p0)
+    rows = np.asarray(rows, dtype=np.int64)
+    out = np.zeros((len(rows), p1 - p0), dtype=bool)
+    cache: dict[tuple[int, int], np.ndarray] = {}
+    for r, p in enumerate(rows):
+        si = next(k for k, s in enumerate(ps) if s.start - p0 <= p < s.start - p0 + s.length)
+        i = (p - (ps[si].start - p0)) // lay.tile
+        if (si, i) not in cache:
+            cache[(si, i)] = _tile_row(lay, la, ca, head, b, si, int(i))
+        out[r] = cache[(si, i)] & (keys <= p)
+    return out
+
+
+# ----------------------------------------------------------------------------
+# Attention (Section 5.2: dense attention restricted to the marked tiles)
+# ----------------------------------------------------------------------------
+
+
+def _kv_head(h: int, hq: int, hkv: int) -> int:
+    return h // (hq // hkv)
+
+
+def masked_softmax_rows(s: np.ndarray, allowed: np.ndarray) -> np.ndarray:
+    """Row softmax of s over the allowed entries only; 0 elsewhere."""
+    s = np.where(allowed, s, -np.inf)
+    mx = s.max(axis=1, keepdims=True)
+    e = np.exp(s - mx)
+    e = np.where(allowed, e, 0.0)
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def _probs_and_mask(lay: Layout, q, k, la, ca, head: int, b: int, rows, scale):
+    hkv = k.shape[1]
+    D = q.shape[2]
+    scale = 1.0 / np.sqrt(D) if scale is None else float(scale)
+    p0, p1 = lay.prompt_span(b)
+    rows = np.asarray(rows, dtype=np.int64)
+    g = _kv_head(head, lay.hq, hkv)
+    qr = np.asarray(q[p0 + rows, head, :], dtype=np.float64)
+    kk = np.asarray(k[p0:p1, g, :], dtype=np.float64)
+    allowed = mask_rows(lay, la, ca, head, b, rows)
+    s = (qr @ kk.T) * scale
+    return masked_softmax_rows(s, allowed), allowed
+
+
+def probabilities(lay: Layout, q, k, la, ca, head: int, b: int, rows, scale=None) -> np.ndarray:
+    """P[r, key] of query head `head` for prompt-relative `rows` of prompt b."""
+    return _probs_and_mask(lay, q, k, la, ca, head, b, rows, scale)[0]
+
+
+def _weighted_rows(P: np.ndarray, allowed: np.ndarray, vv: np.ndarray) -> np.ndarray:
+    """O[r] = sum over the allowed keys of P[r, key] * V[key].  Keys outside
+    the mask are never read, so their V may hold anything, NaN included."""
+    out = np.empty((P.shape[0], vv.shape[1]), dtype=np.float64)
+    for r in range(P.shape[0]):
+        idx = np.nonzero(allowed[r])[0]
+        out[r] = P[r, idx] @ vv[idx]
+    return out
+
+
+def attention(lay: Layout, q, k, v, la, ca, scale=None, heads=None, rows=None) -> np.ndarray:
+    """O[t, h, :] in float64.
+
+    q: [L, Hq, D]; k, v: [L, Hkv, D]; la, ca: uint8 buffers.  With `rows`
+    (global token indices) only those rows are computed and the result is
+    [len(rows), Hq, D]; with `heads` only those heads are filled."""
+    L, hq, D = q.shape
+    heads = range(hq) if heads is None else heads
+    if rows is None:
+        out = np.zeros((L, hq, D), dtype=np.float64)
+        for b in range(lay.num_prompts):
+            p0, p1 = lay.prompt_span(b)
+            vv = {}
+            for h in heads:
+                g = _kv_head(h, hq, k.shape[1])
+                if g not in vv:
+                    vv[g] = np.asarray(v[p0:p1, g, :], dtype=np.float64)
+                for c0 in range(0, p1 - p0, lay.tile):
+                    rr = np.arange(c0, min(c0 + lay.tile, p1 - p0))
+                    P, allowed = _probs_and_mask(lay, q, k, la, ca, h, b, rr, scale)
+                    out[p0 + rr, h, :] = _weighted_rows(P, allowed, vv[g])
+        return out
+    rows = np.asarray(rows, dtype=np.int64)
+    out = np.zeros((len(rows), hq, D), dtype=np.float64)
+    for n, t in enumerate(rows):
+        b = next(bb for bb in range(lay.num_prompts)
+                 if lay.prompt_span(bb)[0] <= t < lay.prompt_span(bb)[1])
+        p0, p1 = lay.prompt_span(b)
+        for h in heads:
+            g = _kv_head(h, hq, k.shape[1])
+            P, allowed = _probs_and_mask(lay, q, k, la, ca, h, b, [t - p0], scale)
+            out[n, h, :] = _weighted_rows(P, allowed, np.asarray(v[p0:p1, g, :], dtype=np.float64))[0]
+    return out
+
+
+# ----------------------------------------------------------------------------
+# Expected decoded lists (Section 5.1), read off the mask
+# ----------------------------------------------------------------------------
+
+
+def _key_tile_any(lay: Layout, b: int, keyrow: np.ndarray) -> list[int]:
+    """Global tile numbers of the prompt's key tiles that hold a True."""
+    p0, _ = lay.prompt_span(b)
+    out = []
+    for s in lay.prompt_segs(b):
+        for i in range(s.pages):
+            lo = s.start - p0 + i * lay.tile
+            hi = s.start - p0 + min((i + 1) * lay.tile, s.length)
+            if keyrow[lo:hi].any():
+                out.append(s.tile_base + i)
+    return out
+
+
+def tile_lists(lay: Layout, la, ca, heads=None, mblocks=None, exhaustive: bool = False):
+    """Expected sparse_n_indices.
+
+    Returns {(h, m): ascending list of global key tiles n such that block
+    (M-block m, N-block n) of head h's mask holds a 1}.  With exhaustive=True
+    every row of the M-block is materialised and OR-ed; otherwise only the
+    block's last row is, which gives the same answer because inside one
+    (M-block, N-block) pair the mask is the same for every row except for the
+    causal cut, which only admits more keys on later rows."""
+    heads = range(lay.hq) if heads is None else heads
+    mblocks = range(lay.num_tiles) if mblocks is None else mblocks
+    res = {}
+    for m in mblocks:
+        seg, i, a, n = lay.tile_span(m)
+        b = seg.prompt
+        p0, _ = lay.prompt_span(b)
+        rows = np.arange(a - p0, a - p0 + n) if exhaustive else np.array([a - p0 + n - 1])
+        for h in heads:
+            msk = mask_rows(lay, la, ca, h, b, rows).any(axis=0)
+            res[(h, m)] = _key_tile_any(lay, b, msk)
+    return res
+
+
+def csr_lists(lay: Layout, la, ca, exhaustive: bool = False):
+    """The lists in packed form: row_ptr[Hq*M+1] (row h*M + m) and col_idx."""
+    lists = tile_lists(lay, la, ca, exhaustive=exhaustive)
+    M = lay.num_tiles
+    row_ptr = np.zeros(lay.hq * M + 1, dtype=np.int64)
+    cols = []
+    for h in range(lay.hq):
+        for m in range(M):
+            lst = lists[(h, m)]
+            row_ptr[h * M + m + 1] = row_ptr[h * M + m] + len(lst)
+            cols.extend(lst)
+    return row_ptr, np.asarray(cols, dtype=np.int64)
+
+
+def useful_flops(lay: Layout, lists: dict, head_dim: int) -> int:
+    """4*D per computed (query, key) cell of the listed tiles: causal cells of
+    the tiles, within segment lengths (QK^T and PV, one multiply-add each)."""
+    total = 0
+    for (h, m), lst in lists.items():
+        _, _, qa, qn = lay.tile_span(m)
+        for n in lst:
+            _, _, ka, kn = lay.tile_span(n)
+            if n == m:
+                total += qn * (qn + 1) // 2
+            else:
+                total += qn * kn
+    return 4 * head_dim * total
