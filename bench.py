@@ -1,0 +1,267 @@
+"""Benchmark of the SIFT sparse prefill hot path on one MI355X.
+
+A step is one layer of the online path for one batch of synthetic input:
+decode the bit vectors into tile lists, then sparse attention over them
+(sift_plan_run).  The default workload is the 64K long-context layer:
+48 query heads / 8 kv heads, head_dim 128, bf16, 32 documents x 2048 tokens
+plus a 512-token query, tile 64, bit vectors at 15% tile density.
+
+Prints one JSON line: useful attention TFLOP/s (4*D flop per computed
+query-key cell), the fraction of the bf16 MFMA peak reached by the attention
+kernel, the speedup over the same kernels with all-ones bit vectors (dense
+causal attention), and the fp64 oracle timed on a sample on the host.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+BF16_PEAK_TFLOPS = 2516.6   # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def tile_tables(seg_offsets, prompt_seg_ptr, tile):
+    """Per global tile: token count and first tile of its prompt (segment-local tiling)."""
+    lens, lo = [], []
+    for b in range(len(prompt_seg_ptr) - 1):
+        first = len(lens)
+        for s in range(prompt_seg_ptr[b], prompt_seg_ptr[b + 1]):
+            n = int(seg_offsets[s + 1] - seg_offsets[s])
+            for i in range(-(-n // tile)):
+                lens.append(min(tile, n - i * tile))
+                lo.append(first)
+    return np.asarray(lens, np.int64), np.asarray(lo, np.int64)
+
+
+def useful_flops(row_ptr, col_idx, tlen, M, D):
+    """4*D per causal in-range cell of every listed (head, M-block, N-block)."""
+    counts = np.diff(row_ptr)
+    m = np.repeat(np.arange(len(counts)) % M, counts)
+    n = col_idx[: len(m)]
+    qn, kn = tlen[m], tlen[n]
+    cells = np.where(n == m, qn * (qn + 1) // 2, qn * kn)
+    return 4 * D * int(cells.sum())
+
+
+def row_cells(rows, heads, row_ptr, col_idx, tlen, tok_tile, tok_local, M):
+    """Computed cells of given (row, head) pairs, from the lists."""
+    total = 0
+    for r in rows:
+        m = tok_tile[r]
+        for h in heads:
+            lst = col_idx[row_ptr[h * M + m]: row_ptr[h * M + m + 1]]
+            total += int(tlen[lst[lst != m]].sum()) + int(tok_local[r]) + 1
+    return total
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="long64k")
+    ap.add_argument("--rho", type=float, default=None)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--only-steps", action="store_true",
+                    help="run warmup + timed steps only (for profiler runs)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the path has no multi-GPU part "
+              f"(--gpus {args.gpus} requested)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import workloads as W
+    from paper_2606_09441_amd import Plan
+
+    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    dev = torch.device("cuda:0")
+    kw = {} if args.rho is None else {"rho": args.rho}
+    t0 = time.time()
+    wl = W.make(args.workload, **kw)
+    log(f"workload {wl.name}: {wl.tokens} tokens, hq={wl.hq} hkv={wl.hkv} D={wl.d} "
+        f"T={wl.tile} (generated in {time.time() - t0:.1f}s)")
+    dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    q = torch.from_numpy(wl.q).to(dev).to(dt)
+    k = torch.from_numpy(wl.k).to(dev).to(dt)
+    v = torch.from_numpy(wl.v).to(dev).to(dt)
+    la = torch.from_numpy(wl.la).to(dev)
+    ca = torch.from_numpy(wl.ca).to(dev)
+    out = torch.empty_like(q)
+    torch.cuda.synchronize()
+
+    tp = time.perf_counter()
+    plan = Plan(wl.seg_offsets, wl.prompt_seg_ptr, wl.hq, wl.hkv, wl.d, wl.tile)
+    plan_ms = (time.perf_counter() - tp) * 1e3
+    M = plan.info["num_tiles"]
+    stream = torch.cuda.current_stream()
+
+    def timed(fn, steps):
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    def per_launch(fn, steps):
+        """Average duration of one launch of fn, events around each launch."""
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(steps)]
+        torch.cuda.synchronize()
+        for a, b in ev:
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        return float(np.mean([a.elapsed_time(b) for a, b in ev]))
+
+    step = lambda: plan.run(q, k, v, la, ca, out=out)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+    ms_step = timed(step, args.steps)
+    log(f"timed {args.steps} steps: {ms_step:.3f} ms/step")
+    if args.only_steps:
+        return
+
+    # lists and useful work of this input
+    rp_t, ci_t = plan.decode(la, ca)
+    torch.cuda.synchronize()
+    rp = rp_t.cpu().numpy().astype(np.int64)
+    ci = ci_t[: int(rp[-1])].cpu().numpy().astype(np.int64)
+    tlen, _ = tile_tables(wl.seg_offsets, wl.prompt_seg_ptr, wl.tile)
+    flops = useful_flops(rp, ci, tlen, M, wl.d)
+    nnz = int(rp[-1])
+    density = nnz / plan.info["list_capacity"]
+    ms_decode = per_launch(lambda: plan.decode(la, ca, rp_t, ci_t), args.steps)
+    ms_attn = per_launch(lambda: plan.attention(q, k, v, rp_t, ci_t, out=out), args.steps)
+    log(f"decode {ms_decode * 1e3:.1f} us, attention {ms_attn:.3f} ms, nnz {nnz}, "
+        f"density {density:.4f}, useful {flops / 1e12:.3f} TFLOP")
+
+    dense = {}
+    if not args.no_dense:
+        wd = W.all_ones(wl)
+        la_d = torch.from_numpy(wd.la).to(dev)
+        ca_d = torch.from_numpy(wd.ca).to(dev)
+        step_d = lambda: plan.run(q, k, v, la_d, ca_d, out=out)
+        for _ in range(max(1, args.warmup)):
+            step_d()
+        ms_step_d = timed(step_d, max(2, args.steps // 2))
+        rpd, cid = plan.decode(la_d, ca_d)
+        ms_attn_d = per_launch(lambda: plan.attention(q, k, v, rpd, cid, out=out),
+                               max(2, args.steps // 2))
+        torch.cuda.synchronize()
+        rpd_h = rpd.cpu().numpy().astype(np.int64)
+        flops_d = useful_flops(rpd_h, cid[: int(rpd_h[-1])].cpu().numpy().astype(np.int64),
+                               tlen, M, wl.d)
+        dense = {
+            "ms_per_step": round(ms_step_d, 4),
+            "attention_ms": round(ms_attn_d, 4),
+            "useful_tflops": round(flops_d / ms_attn_d / 1e9, 2),
+            "speedup_step": round(ms_step_d / ms_step, 3),
+            "speedup_attention": round(ms_attn_d / ms_attn, 3),
+            "inverse_density": round(1.0 / density, 3),
+        }
+        log(f"dense: step {ms_step_d:.3f} ms, attention {ms_attn_d:.3f} ms "
+            f"({flops_d / ms_attn_d / 1e9:.1f} TFLOP/s); speedup {ms_step_d / ms_step:.2f}x "
+            f"vs 1/density {1 / density:.2f}")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import sift_oracle as O
+        try:
+            from threadpoolctl import threadpool_info
+            threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        except Exception:
+            threads = 1
+        lay = O.Layout(wl.seg_offsets, wl.prompt_seg_ptr, wl.tile, wl.hq)
+        tok_tile = np.zeros(wl.tokens, np.int64)
+        tok_local = np.zeros(wl.tokens, np.int64)
+        for s in lay.segs:
+            loc = np.arange(s.length)
+            tok_tile[s.start:s.start + s.length] = s.tile_base + loc // wl.tile
+            tok_local[s.start:s.start + s.length] = loc % wl.tile
+        rng = np.random.default_rng(0)
+        order = rng.permutation(wl.tokens)
+        done, cells, t_cpu = 0, 0, 0.0
+        while t_cpu < args.cpu_seconds and done < wl.tokens:
+            rows = np.sort(order[done:done + 8])
+            tc = time.perf_counter()
+            O.attention(lay, wl.q, wl.k, wl.v, wl.la, wl.ca, rows=rows)
+            t_cpu += time.perf_counter() - tc
+            cells += row_cells(rows, range(wl.hq), rp, ci, tlen, tok_tile, tok_local, M)
+            done += len(rows)
+        cpu = {
+            "value": round(4 * wl.d * cells / t_cpu / 1e12, 6),
+            "unit": "TFLOP/s",
+            "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{done} random query rows x all {wl.hq} heads of the same input "
+                      f"({t_cpu:.1f}s, fp64 numpy)",
+        }
+        log(f"cpu oracle: {cpu['value']} TFLOP/s on {done} rows in {t_cpu:.1f}s")
+
+    achieved = flops / ms_attn / 1e9
+    res = {
+        "metric": "useful attention TFLOP/s (sparse prefill, decode + attention)",
+        "value": round(flops / ms_step / 1e9, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name}: {wl.tokens} tokens ({len(wl.seg_offsets) - 2} docs + query), "
+                        f"{wl.hq}/{wl.hkv} heads, D={wl.d}, T={wl.tile}",
+            "tokens": wl.tokens, "q_heads": wl.hq, "kv_heads": wl.hkv, "head_dim": wl.d,
+            "tile": wl.tile, "rho": wl.meta.get("rho"),
+        },
+        "density": round(density, 5),
+        "nnz_tiles": nnz,
+        "useful_tflop_per_step": round(flops / 1e12, 4),
+        "decode_us": round(ms_decode * 1e3, 2),
+        "attention_ms": round(ms_attn, 4),
+        "plan_ms": round(plan_ms, 3),
+        "pct_bf16_peak_attention": round(100 * achieved / BF16_PEAK_TFLOPS, 2),
+        "dense": dense or None,
+        "roofline": {
+            "bound": "mfma",
+            "achieved": round(achieved, 2),
+            "peak": BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
+            "traffic": None,
+        },
+        "cpu_baseline": cpu,
+    }
+    plan.close()
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

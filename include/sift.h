@@ -1,0 +1,206 @@
+/*
+ * sift.h - C ABI of libsift: bitmap-driven sparse prefill attention for
+ * AMD Instinct MI355X (gfx950), after SIFT (arXiv 2606.09441).
+ *
+ * One call computes, for one layer, causal GQA attention of a packed batch
+ * of RAG prompts, evaluating only the tiles that two bit vectors per
+ * (document, query head) mark (Sections 4.1-4.2), with the user-query rows
+ * dense (Section 3.1).  It runs as two device steps (Section 5):
+ *   1. decode: the bit vectors become, for every (query head, M-block), a
+ *      packed ascending int32 list of the key tiles (N-blocks) to compute
+ *      (Section 5.1, "sparse_n_indices"): a count pass, a prefix sum, a
+ *      write pass;
+ *   2. attention: a flash-style kernel walks only the listed tiles with an
+ *      online softmax (Section 5.2).
+ *
+ * Conventions used by every entry point
+ * -------------------------------------
+ * Tensors: q, out are [tokens][Hq][D], k, v are [tokens][Hkv][D], dense,
+ *   row-major, in device memory.  Query head h reads kv head h / (Hq/Hkv).
+ * Layout (host memory): prompt b owns segments prompt_seg_ptr[b] ..
+ *   prompt_seg_ptr[b+1]-1 of the packed token axis; the last one is its user
+ *   query, the ones before it its documents in prompt order.  Segment s
+ *   covers tokens seg_offsets[s] .. seg_offsets[s+1]-1.  Documents hold at
+ *   least one token; a query may be empty.  Prompts never attend to each
+ *   other.
+ * Tiles: tile size T.  Tiles are segment-local: tile i of segment s covers
+ *   tokens seg_offsets[s] + i*T .. + T-1, clipped to the segment, so the last
+ *   tile of a segment may be partial.  P_s = ceil(len_s / T) (Section 4.3).
+ *   The global number of tile i of segment s is i plus the tile count of all
+ *   earlier segments (of all prompts); M is the total.  Every tile is both
+ *   an M-block (query rows) and an N-block (keys).
+ * Bit vectors (device memory, Sections 4.1-4.3): local_bitmap holds, for
+ *   every document of every prompt in layout order and, inside it, for query
+ *   heads h = 0..Hq-1, ceil(P(P+1)/16) bytes: one bit per tile (i, j), j <= i,
+ *   of the document's lower triangle, enumerated (0,0),(1,0),(1,1),(2,0),...,
+ *   most significant bit first.  cross_bitmap holds, in the same order,
+ *   ceil(P/8) bytes per vector: bit p (MSB first) says whether key page p of
+ *   the document is computed for the rows of later documents of the prompt.
+ *   Stored diagonal bits and padding bits are ignored: diagonal tiles are
+ *   always computed.
+ * Lists: row h*M + m of row_ptr/col_idx holds query head h, M-block m.
+ *   Document M-block i of document d lists, in ascending order, the marked
+ *   pages of every earlier document of its prompt, the marked tiles j < i of
+ *   d, then i itself.  A query M-block lists every tile of its prompt up to
+ *   and including itself.
+ * Streams: `stream` is a hipStream_t (NULL = the null stream).  All device
+ *   work is enqueued on it; entry points return once it is enqueued.
+ * Errors: arguments are checked on the host before anything is enqueued; on
+ *   any error nothing is written and nothing is enqueued.  SIFT_E_HIP
+ *   reports a failed HIP call; faults of enqueued kernels surface at the
+ *   caller's next synchronisation.
+ * Threads: plans are not shared between concurrent calls: calls that use
+ *   the same plan must be ordered (same stream, or synchronised), since they
+ *   share the plan's device scratch.
+ */
+#ifndef SIFT_H_
+#define SIFT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum sift_status {
+  SIFT_OK = 0,
+  SIFT_E_NULL = 1,        /* a required pointer is NULL                       */
+  SIFT_E_SHAPE = 2,       /* tensor shapes disagree (with each other/layout)  */
+  SIFT_E_LAYOUT = 3,      /* malformed layout                                 */
+  SIFT_E_UNSUPPORTED = 4, /* valid, but outside this build (tile, D, dtype)   */
+  SIFT_E_CAPACITY = 5,    /* a caller buffer is too small                     */
+  SIFT_E_HIP = 6,         /* a HIP runtime call failed                        */
+  SIFT_E_PLAN = 7         /* the plan does not match the arguments            */
+} sift_status;
+
+typedef enum sift_dtype { SIFT_F32 = 0, SIFT_BF16 = 1 } sift_dtype;
+
+/* A dense device tensor [tokens][heads][head_dim]. */
+typedef struct sift_tensor {
+  void* data;
+  int32_t dtype; /* sift_dtype */
+  int32_t tokens;
+  int32_t heads;
+  int32_t head_dim;
+} sift_tensor;
+
+/* The prompt layout, in host memory; see "Layout" above. */
+typedef struct sift_layout {
+  int32_t num_prompts;            /* B >= 1                                  */
+  const int32_t* prompt_seg_ptr;  /* [B + 1], prompt_seg_ptr[0] == 0         */
+  const int32_t* seg_offsets;     /* [prompt_seg_ptr[B] + 1], [0] == 0       */
+} sift_layout;
+
+/* Opaque: a validated layout, its device tables and scratch. */
+typedef struct sift_plan sift_plan;
+
+typedef struct sift_plan_info {
+  int32_t num_tokens;
+  int32_t num_segments;
+  int32_t num_tiles;        /* M                                            */
+  int32_t num_q_heads;      /* Hq                                           */
+  int32_t num_kv_heads;     /* Hkv                                          */
+  int32_t head_dim;         /* D                                            */
+  int32_t tile;             /* T                                            */
+  int32_t num_work_units;   /* attention work units (head, M-block pair)    */
+  int64_t num_rows;         /* Hq * M; row_ptr holds num_rows + 1 entries   */
+  int64_t list_capacity;    /* Hq * (dense causal tile count): >= any nnz   */
+  int64_t la_bytes;         /* size local_bitmap must have                  */
+  int64_t ca_bytes;         /* size cross_bitmap must have                  */
+  int64_t scratch_bytes;    /* device memory the plan holds                 */
+} sift_plan_info;
+
+/* Human-readable name of a status code.  Never NULL. */
+const char* sift_status_string(int32_t status);
+
+/*
+ * Validate a layout and build a plan for it (Sections 4.3, 5.1: page counts,
+ * bit-vector offsets, tile numbering, the (head, M-block) work units).
+ * Allocates device memory on the current device (the tables, and scratch
+ * for the decoded lists of sift_plan_run) and uploads the tables
+ * synchronously.  A plan is reusable for every layer of the same prompts.
+ *   layout           host layout, read only during the call
+ *   num_q_heads      Hq >= 1;  num_kv_heads: Hkv >= 1, Hq % Hkv == 0
+ *   head_dim         D: 64 or 128
+ *   tile             T: 16, 32 or 64
+ *   plan_out         receives the plan; the caller frees it with
+ *                    sift_plan_destroy.
+ * Errors: SIFT_E_NULL, SIFT_E_LAYOUT, SIFT_E_SHAPE, SIFT_E_UNSUPPORTED,
+ *         SIFT_E_CAPACITY (more than 2^31-1 list entries), SIFT_E_HIP.
+ */
+sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
+                             int32_t num_kv_heads, int32_t head_dim,
+                             int32_t tile, sift_plan** plan_out);
+
+/* Free a plan and its device memory (synchronises the device first).
+ * NULL is accepted. */
+sift_status sift_plan_destroy(sift_plan* plan);
+
+/* Copy the plan's sizes into *info. */
+sift_status sift_plan_get_info(const sift_plan* plan, sift_plan_info* info);
+
+/*
+ * Decoding (Section 5.1): expand the bit vectors into the packed lists.
+ *   local_bitmap, cross_bitmap   device, la_bytes / ca_bytes of the plan
+ *   row_ptr      device int32 [num_rows + 1], written: exclusive prefix sum
+ *                of the per-row counts; row_ptr[num_rows] = nnz
+ *   col_idx      device int32 [col_capacity], written: entries 0 .. nnz-1
+ *   col_capacity must be >= the plan's list_capacity (an upper bound of nnz
+ *                known on the host), else SIFT_E_CAPACITY.
+ * Uses the plan's scratch for the counts.
+ */
+sift_status sift_decode_tiles(sift_plan* plan, const uint8_t* local_bitmap,
+                              const uint8_t* cross_bitmap, int32_t* row_ptr,
+                              int32_t* col_idx, int64_t col_capacity,
+                              void* stream);
+
+/*
+ * Sparse attention (Section 5.2) over given lists: for every (h, M-block m),
+ * out rows of m = softmax over the keys of the listed tiles (causal inside
+ * the diagonal tile, length-masked in partial tiles) times V.
+ *   q, k, v      device tensors; dtype both SIFT_BF16 (needs T = 64 and
+ *                D = 128: MFMA kernel) or both SIFT_F32 (any supported T, D)
+ *   row_ptr, col_idx   device lists in the format sift_decode_tiles writes,
+ *                col_capacity entries of col_idx readable.  Entries outside
+ *                the M-block's prompt or after the M-block are skipped;
+ *                lists must be ascending.  A row whose list is empty gets 0.
+ *   softmax_scale  <= 0 selects 1/sqrt(D)
+ *   out          device tensor [tokens][Hq][D], SIFT_BF16 or SIFT_F32 for
+ *                bf16 inputs, SIFT_F32 for fp32 inputs.
+ */
+sift_status sift_sparse_attention(sift_plan* plan, const sift_tensor* q,
+                                  const sift_tensor* k, const sift_tensor* v,
+                                  const int32_t* row_ptr,
+                                  const int32_t* col_idx, int64_t col_capacity,
+                                  float softmax_scale, sift_tensor* out,
+                                  void* stream);
+
+/*
+ * One layer of the online hot path: decode into the plan's own list
+ * scratch, then sparse attention (Sections 5.1 and 5.2).  No allocation.
+ */
+sift_status sift_plan_run(sift_plan* plan, const sift_tensor* q,
+                          const sift_tensor* k, const sift_tensor* v,
+                          const uint8_t* local_bitmap,
+                          const uint8_t* cross_bitmap, float softmax_scale,
+                          sift_tensor* out, void* stream);
+
+/*
+ * One-shot form with the arguments of the paper's problem statement: Q, K,
+ * V of one layer, the document layout, the two bit vectors and the tile
+ * size (Sections 4 and 5).  Builds a plan, runs it on `stream` with scale
+ * 1/sqrt(D), waits for the stream, and frees the plan.
+ */
+sift_status sift_sparse_prefill(const sift_tensor* q, const sift_tensor* k,
+                                const sift_tensor* v,
+                                const sift_layout* doc_offsets,
+                                const uint8_t* local_bitmap,
+                                const uint8_t* cross_bitmap, int32_t tile,
+                                sift_tensor* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SIFT_H_ */

@@ -164,35 +164,50 @@ class Layout:
 # ----------------------------------------------------------------------------
 
 
-def _tile_row(lay: Layout, la, ca, head: int, b: int, seg_index: int, i: int) -> np.ndarray:
+def _page_bits(buf, off: int, n: int) -> np.ndarray:
+    return np.array([read_bit(buf, off, b) for b in range(n)], dtype=bool)
+
+
+def _tile_row(lay: Layout, la, ca, head: int, b: int, seg_index: int, i: int,
+              cache: dict | None = None) -> np.ndarray:
     """Key visibility for every row of tile i of segment seg_index (prompt b),
-    before the causal cut: one bool per token of the prompt."""
+    before the causal cut: one bool per token of the prompt.  `cache` may
+    hold the part that depends only on (head, prompt, segment): the keys of
+    earlier documents."""
     ps = lay.prompt_segs(b)
     p0, p1 = lay.prompt_span(b)
-    row = np.zeros(p1 - p0, dtype=bool)
     me = ps[seg_index]
-    for si, se in enumerate(ps):
-        a = se.start - p0
-        if me.is_query:
-            # the user query recomputes everything before it (Section 3.1)
-            row[a:a + se.length] = True
-        elif si < seg_index:
-            # cross attention: page p of an earlier document (Section 4.2)
-            off = se.ca_offset + head * ca_num_bytes(se.pages)
-            for page in range(se.pages):
-                lo, hi = page * lay.tile, min((page + 1) * lay.tile, se.length)
-                row[a + lo:a + hi] = bool(read_bit(ca, off, page))
-        elif si == seg_index:
-            # local attention: tiles j <= i of the same document (Section 4.1)
-            off = se.la_offset + head * la_num_bytes(se.pages)
-            for j in range(i + 1):
-                bit = 1 if j == i else read_bit(la, off, la_bit_position(i, j))
-                lo, hi = j * lay.tile, min((j + 1) * lay.tile, se.length)
-                row[a + lo:a + hi] = bool(bit)
+    key = (head, b, seg_index)
+    if cache is not None and key in cache:
+        row = cache[key].copy()
+    else:
+        row = np.zeros(p1 - p0, dtype=bool)
+        for si, se in enumerate(ps[:seg_index]):
+            a = se.start - p0
+            if me.is_query:
+                # the user query recomputes everything before it (Section 3.1)
+                row[a:a + se.length] = True
+            else:
+                # cross attention: page p of an earlier document (Section 4.2)
+                off = se.ca_offset + head * ca_num_bytes(se.pages)
+                bits = _page_bits(ca, off, se.pages)
+                row[a:a + se.length] = np.repeat(bits, lay.tile)[:se.length]
+        if cache is not None:
+            cache[key] = row.copy()
+    a = me.start - p0
+    if me.is_query:
+        row[a:a + me.length] = True
+    else:
+        # local attention: tiles j <= i of the same document (Section 4.1)
+        off = me.la_offset + head * la_num_bytes(me.pages)
+        for j in range(i + 1):
+            bit = 1 if j == i else read_bit(la, off, la_bit_position(i, j))
+            lo, hi = j * lay.tile, min((j + 1) * lay.tile, me.length)
+            row[a + lo:a + hi] = bool(bit)
     return row
 
 
-def mask_rows(lay: Layout, la, ca, head: int, b: int, rows) -> np.ndarray:
+def mask_rows(lay: Layout, la, ca, head: int, b: int, rows, cache: dict | None = None) -> np.ndarray:
     """allowed[r, k] for the prompt-relative query tokens `rows` of prompt b
     against every key token of that prompt, for query head `head`."""
     ps = lay.prompt_segs(b)
@@ -200,13 +215,13 @@ def mask_rows(lay: Layout, la, ca, head: int, b: int, rows) -> np.ndarray:
     keys = np.arange(p1 - p0)
     rows = np.asarray(rows, dtype=np.int64)
     out = np.zeros((len(rows), p1 - p0), dtype=bool)
-    cache: dict[tuple[int, int], np.ndarray] = {}
+    cache_rows: dict[tuple[int, int], np.ndarray] = {}
     for r, p in enumerate(rows):
         si = next(k for k, s in enumerate(ps) if s.start - p0 <= p < s.start - p0 + s.length)
         i = (p - (ps[si].start - p0)) // lay.tile
-        if (si, i) not in cache:
-            cache[(si, i)] = _tile_row(lay, la, ca, head, b, si, int(i))
-        out[r] = cache[(si, i)] & (keys <= p)
+        if (si, i) not in cache_rows:
+            cache_rows[(si, i)] = _tile_row(lay, la, ca, head, b, si, int(i), cache)
+        out[r] = cache_rows[(si, i)] & (keys <= p)
     return out
 
 
@@ -300,14 +315,15 @@ def attention(lay: Layout, q, k, v, la, ca, scale=None, heads=None, rows=None) -
 def _key_tile_any(lay: Layout, b: int, keyrow: np.ndarray) -> list[int]:
     """Global tile numbers of the prompt's key tiles that hold a True."""
     p0, _ = lay.prompt_span(b)
-    out = []
+    starts, ids = [], []
     for s in lay.prompt_segs(b):
         for i in range(s.pages):
-            lo = s.start - p0 + i * lay.tile
-            hi = s.start - p0 + min((i + 1) * lay.tile, s.length)
-            if keyrow[lo:hi].any():
-                out.append(s.tile_base + i)
-    return out
+            starts.append(s.start - p0 + i * lay.tile)
+            ids.append(s.tile_base + i)
+    if not starts:
+        return []
+    hit = np.logical_or.reduceat(keyrow, np.asarray(starts))
+    return [n for n, x in zip(ids, hit) if x]
 
 
 def tile_lists(lay: Layout, la, ca, heads=None, mblocks=None, exhaustive: bool = False):
@@ -322,13 +338,14 @@ def tile_lists(lay: Layout, la, ca, heads=None, mblocks=None, exhaustive: bool =
     heads = range(lay.hq) if heads is None else heads
     mblocks = range(lay.num_tiles) if mblocks is None else mblocks
     res = {}
+    cache: dict = {}
     for m in mblocks:
         seg, i, a, n = lay.tile_span(m)
         b = seg.prompt
         p0, _ = lay.prompt_span(b)
         rows = np.arange(a - p0, a - p0 + n) if exhaustive else np.array([a - p0 + n - 1])
         for h in heads:
-            msk = mask_rows(lay, la, ca, h, b, rows).any(axis=0)
+            msk = mask_rows(lay, la, ca, h, b, rows, cache).any(axis=0)
             res[(h, m)] = _key_tile_any(lay, b, msk)
     return res
 

@@ -1,0 +1,17 @@
+"""SIFT sparse prefill attention for AMD Instinct MI355X (gfx950).
+
+The compute path is libsift.so (HIP kernels + C ABI, include/sift.h); this
+package only marshals torch tensors into it.  Importing the package does not
+load the library; the first call does, and fails loudly if it is not built.
+"""
+
+from ._lib import (  # noqa: F401
+    Plan,
+    SiftError,
+    default_scale,
+    header_functions,
+    lib,
+    sparse_prefill,
+)
+
+__all__ = ["Plan", "SiftError", "sparse_prefill", "lib", "header_functions", "default_scale"]

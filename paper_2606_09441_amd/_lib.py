@@ -1,0 +1,232 @@
+"""ctypes binding of libsift (include/sift.h).  Marshalling only: every step
+of the hot path runs in the library's HIP kernels; torch provides device
+memory and the current stream."""
+
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsift.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "sift.h")
+
+SIFT_F32 = 0
+SIFT_BF16 = 1
+
+STATUS = {
+    0: "SIFT_OK", 1: "SIFT_E_NULL", 2: "SIFT_E_SHAPE", 3: "SIFT_E_LAYOUT",
+    4: "SIFT_E_UNSUPPORTED", 5: "SIFT_E_CAPACITY", 6: "SIFT_E_HIP", 7: "SIFT_E_PLAN",
+}
+
+
+class SiftError(RuntimeError):
+    def __init__(self, fn: str, status: int, msg: str):
+        super().__init__(f"{fn}: {STATUS.get(status, status)} ({msg})")
+        self.status = status
+
+
+class SiftTensor(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("dtype", ctypes.c_int32), ("tokens", ctypes.c_int32),
+                ("heads", ctypes.c_int32), ("head_dim", ctypes.c_int32)]
+
+
+class SiftLayout(ctypes.Structure):
+    _fields_ = [("num_prompts", ctypes.c_int32),
+                ("prompt_seg_ptr", ctypes.POINTER(ctypes.c_int32)),
+                ("seg_offsets", ctypes.POINTER(ctypes.c_int32))]
+
+
+class SiftPlanInfo(ctypes.Structure):
+    _fields_ = [("num_tokens", ctypes.c_int32), ("num_segments", ctypes.c_int32),
+                ("num_tiles", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("tile", ctypes.c_int32), ("num_work_units", ctypes.c_int32),
+                ("num_rows", ctypes.c_int64), ("list_capacity", ctypes.c_int64),
+                ("la_bytes", ctypes.c_int64), ("ca_bytes", ctypes.c_int64),
+                ("scratch_bytes", ctypes.c_int64)]
+
+
+_P = ctypes.c_void_p
+_SIGS = {
+    "sift_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
+    "sift_plan_create": (ctypes.c_int, [ctypes.POINTER(SiftLayout), ctypes.c_int32, ctypes.c_int32,
+                                        ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(_P)]),
+    "sift_plan_destroy": (ctypes.c_int, [_P]),
+    "sift_plan_get_info": (ctypes.c_int, [_P, ctypes.POINTER(SiftPlanInfo)]),
+    "sift_decode_tiles": (ctypes.c_int, [_P, _P, _P, _P, _P, ctypes.c_int64, _P]),
+    "sift_sparse_attention": (ctypes.c_int, [_P, ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftTensor),
+                                             ctypes.POINTER(SiftTensor), _P, _P, ctypes.c_int64,
+                                             ctypes.c_float, ctypes.POINTER(SiftTensor), _P]),
+    "sift_plan_run": (ctypes.c_int, [_P, ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftTensor),
+                                     ctypes.POINTER(SiftTensor), _P, _P, ctypes.c_float,
+                                     ctypes.POINTER(SiftTensor), _P]),
+    "sift_sparse_prefill": (ctypes.c_int, [ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftTensor),
+                                           ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftLayout),
+                                           _P, _P, ctypes.c_int32, ctypes.POINTER(SiftTensor), _P]),
+}
+
+_lib = None
+
+
+def header_functions() -> list[str]:
+    """Names of the functions include/sift.h declares."""
+    with open(HEADER) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sift_[a-z_]+)\s*\(", text)))
+
+
+def lib() -> ctypes.CDLL:
+    """Load libsift.so once.  Raises if it has not been built: there is no
+    fallback path."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2606_09441_amd.build` (no fallback exists)")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def check(fn: str, status: int) -> None:
+    if status != 0:
+        msg = lib().sift_status_string(status).decode()
+        raise SiftError(fn, status, msg)
+
+
+# ----------------------------------------------------------------------------
+# torch marshalling
+# ----------------------------------------------------------------------------
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def tensor_desc(t) -> SiftTensor:
+    torch = _torch()
+    if t.dim() != 3:
+        raise ValueError("expected a [tokens, heads, head_dim] tensor")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    if t.dtype == torch.bfloat16:
+        dt = SIFT_BF16
+    elif t.dtype == torch.float32:
+        dt = SIFT_F32
+    else:
+        raise ValueError(f"unsupported dtype {t.dtype}")
+    return SiftTensor(t.data_ptr(), dt, t.shape[0], t.shape[1], t.shape[2])
+
+
+def layout_struct(seg_offsets, prompt_seg_ptr):
+    so = np.ascontiguousarray(np.asarray(seg_offsets, dtype=np.int32))
+    ps = np.ascontiguousarray(np.asarray(prompt_seg_ptr, dtype=np.int32))
+    lay = SiftLayout(len(ps) - 1, ps.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                     so.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)))
+    return lay, (so, ps)  # keep the arrays alive with the struct
+
+
+def _stream_ptr(stream):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(0 if t is None else t.data_ptr())
+
+
+class Plan:
+    """A validated prompt layout with its device tables (sift_plan_*)."""
+
+    def __init__(self, seg_offsets, prompt_seg_ptr, num_q_heads, num_kv_heads, head_dim, tile=64):
+        self._h = None
+        lay, keep = layout_struct(seg_offsets, prompt_seg_ptr)
+        h = ctypes.c_void_p()
+        check("sift_plan_create", lib().sift_plan_create(ctypes.byref(lay), num_q_heads, num_kv_heads,
+                                                         head_dim, tile, ctypes.byref(h)))
+        self._h = h
+        inf = SiftPlanInfo()
+        check("sift_plan_get_info", lib().sift_plan_get_info(self._h, ctypes.byref(inf)))
+        self.info = {name: getattr(inf, name) for name, _ in SiftPlanInfo._fields_}
+
+    def close(self):
+        if self._h is not None:
+            check("sift_plan_destroy", lib().sift_plan_destroy(self._h))
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def decode(self, la, ca, row_ptr=None, col_idx=None, stream=None):
+        """Decoded lists (Section 5.1) as device int32 tensors (row_ptr, col_idx)."""
+        torch = _torch()
+        dev = la.device
+        if row_ptr is None:
+            row_ptr = torch.empty(self.info["num_rows"] + 1, dtype=torch.int32, device=dev)
+        if col_idx is None:
+            col_idx = torch.empty(max(1, self.info["list_capacity"]), dtype=torch.int32, device=dev)
+        check("sift_decode_tiles", lib().sift_decode_tiles(
+            self._h, _ptr(la), _ptr(ca), _ptr(row_ptr), _ptr(col_idx), col_idx.numel(),
+            _stream_ptr(stream)))
+        return row_ptr, col_idx
+
+    def attention(self, q, k, v, row_ptr, col_idx, scale=None, out=None, out_dtype=None, stream=None):
+        """Sparse attention over given lists (Section 5.2)."""
+        torch = _torch()
+        if out is None:
+            out = torch.empty(q.shape, dtype=out_dtype or q.dtype, device=q.device)
+        qd, kd, vd, od = tensor_desc(q), tensor_desc(k), tensor_desc(v), tensor_desc(out)
+        check("sift_sparse_attention", lib().sift_sparse_attention(
+            self._h, ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), _ptr(row_ptr),
+            _ptr(col_idx), col_idx.numel(), ctypes.c_float(0.0 if scale is None else scale),
+            ctypes.byref(od), _stream_ptr(stream)))
+        return out
+
+    def run(self, q, k, v, la, ca, scale=None, out=None, out_dtype=None, stream=None):
+        """Decode + attention for one layer (sift_plan_run)."""
+        torch = _torch()
+        if out is None:
+            out = torch.empty(q.shape, dtype=out_dtype or q.dtype, device=q.device)
+        qd, kd, vd, od = tensor_desc(q), tensor_desc(k), tensor_desc(v), tensor_desc(out)
+        check("sift_plan_run", lib().sift_plan_run(
+            self._h, ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), _ptr(la), _ptr(ca),
+            ctypes.c_float(0.0 if scale is None else scale), ctypes.byref(od), _stream_ptr(stream)))
+        return out
+
+
+def sparse_prefill(q, k, v, seg_offsets, prompt_seg_ptr, la, ca, tile=64, out=None, stream=None):
+    """One-shot sift_sparse_prefill: plan, decode, attention, wait, free."""
+    torch = _torch()
+    if out is None:
+        out = torch.empty_like(q)
+    lay, keep = layout_struct(seg_offsets, prompt_seg_ptr)
+    qd, kd, vd, od = tensor_desc(q), tensor_desc(k), tensor_desc(v), tensor_desc(out)
+    check("sift_sparse_prefill", lib().sift_sparse_prefill(
+        ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), ctypes.byref(lay), _ptr(la), _ptr(ca),
+        tile, ctypes.byref(od), _stream_ptr(stream)))
+    return out
+
+
+def default_scale(head_dim: int) -> float:
+    return 1.0 / math.sqrt(head_dim)

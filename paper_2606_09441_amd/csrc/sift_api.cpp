@@ -1,0 +1,447 @@
+// Host side of libsift: argument checks, the plan (tables derived from the
+// prompt layout, Sections 4.3 and 5.1), the attention schedule, and the
+// C ABI declared in include/sift.h.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <limits>
+#include <new>
+#include <numeric>
+#include <vector>
+
+#include "sift.h"
+#include "sift_internal.h"
+
+namespace {
+
+constexpr int kNumXcd = 8;  // MI355X: workgroups are dealt round-robin over 8 XCDs
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+int64_t la_nbytes(int64_t P) { return ceil_div(P * (P + 1), 16); }  // Section 4.3
+int64_t ca_nbytes(int64_t P) { return ceil_div(P, 8); }             // Section 4.3
+
+}  // namespace
+
+struct sift_plan {
+  int device = 0;
+  sift_plan_info info{};
+  // one device allocation holds every table, then the decode scratch
+  void* dev = nullptr;
+  size_t dev_bytes = 0;
+  sift::PlanTables pt{};
+  sift::WorkTables wt{};
+  int32_t* counts = nullptr;   // [num_rows]
+  int32_t* row_ptr = nullptr;  // [num_rows + 1]
+  int32_t* col_idx = nullptr;  // [list_capacity]
+};
+
+namespace {
+
+sift_status check_tensor(const sift_tensor* t, int32_t tokens, int32_t heads, int32_t dim) {
+  if (t == nullptr) return SIFT_E_NULL;
+  if (t->data == nullptr && static_cast<int64_t>(t->tokens) * t->heads * t->head_dim > 0)
+    return SIFT_E_NULL;
+  if (t->dtype != SIFT_F32 && t->dtype != SIFT_BF16) return SIFT_E_UNSUPPORTED;
+  if (t->tokens != tokens || t->heads != heads || t->head_dim != dim) return SIFT_E_SHAPE;
+  return SIFT_OK;
+}
+
+sift_status check_device(const sift_plan* plan) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return SIFT_E_HIP;
+  return dev == plan->device ? SIFT_OK : SIFT_E_PLAN;
+}
+
+// Shapes and dtypes of one call against the plan's sizes.
+sift_status check_io(const sift_tensor* q, const sift_tensor* k, const sift_tensor* v,
+                     const sift_tensor* out, int32_t tokens, int32_t hq, int32_t hkv, int32_t dim,
+                     int32_t tile) {
+  sift_status st;
+  if ((st = check_tensor(q, tokens, hq, dim)) != SIFT_OK) return st;
+  if ((st = check_tensor(k, tokens, hkv, dim)) != SIFT_OK) return st;
+  if ((st = check_tensor(v, tokens, hkv, dim)) != SIFT_OK) return st;
+  if ((st = check_tensor(out, tokens, hq, dim)) != SIFT_OK) return st;
+  if (q->dtype != k->dtype || q->dtype != v->dtype) return SIFT_E_UNSUPPORTED;
+  if (q->dtype == SIFT_BF16 && (tile != 64 || dim != 128)) return SIFT_E_UNSUPPORTED;
+  if (q->dtype == SIFT_F32 && out->dtype != SIFT_F32) return SIFT_E_UNSUPPORTED;
+  return SIFT_OK;
+}
+
+// Host tables of a validated layout.
+struct HostPlan {
+  std::vector<int32_t> seg_tile0, seg_pages, seg_kind, seg_first, seg_la_off, seg_ca_off;
+  std::vector<int32_t> tile_seg, tile_tok0, tile_len, tile_lo;
+  std::vector<int32_t> unit_head, unit_m0, unit_m1, sched;
+  int64_t dense_tiles = 0;  // causal tiles of all prompts, one head
+  int64_t la_bytes = 0, ca_bytes = 0;
+  int32_t num_tokens = 0, num_segments = 0, num_tiles = 0;
+};
+
+sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int32_t tile,
+                            HostPlan& hp) {
+  if (lay->num_prompts < 1) return SIFT_E_LAYOUT;
+  if (lay->prompt_seg_ptr == nullptr || lay->seg_offsets == nullptr) return SIFT_E_NULL;
+  const int32_t B = lay->num_prompts;
+  const int32_t* psp = lay->prompt_seg_ptr;
+  const int32_t* so = lay->seg_offsets;
+  if (psp[0] != 0) return SIFT_E_LAYOUT;
+  for (int32_t b = 0; b < B; ++b)
+    if (psp[b + 1] <= psp[b]) return SIFT_E_LAYOUT;  // every prompt has its query segment
+  const int32_t S = psp[B];
+  if (so[0] != 0) return SIFT_E_LAYOUT;
+  for (int32_t s = 0; s < S; ++s)
+    if (so[s + 1] < so[s]) return SIFT_E_LAYOUT;
+  hp.num_segments = S;
+  hp.num_tokens = so[S];
+  hp.seg_tile0.resize(S);
+  hp.seg_pages.resize(S);
+  hp.seg_kind.resize(S);
+  hp.seg_first.resize(S);
+  hp.seg_la_off.resize(S);
+  hp.seg_ca_off.resize(S);
+  int64_t tiles = 0, la_off = 0, ca_off = 0, dense = 0;
+  const int64_t i32max = std::numeric_limits<int32_t>::max();
+  for (int32_t b = 0; b < B; ++b) {
+    const int64_t lo = tiles;
+    for (int32_t s = psp[b]; s < psp[b + 1]; ++s) {
+      const bool is_query = s == psp[b + 1] - 1;
+      const int64_t len = static_cast<int64_t>(so[s + 1]) - so[s];
+      if (!is_query && len < 1) return SIFT_E_LAYOUT;  // documents are not empty
+      const int64_t P = ceil_div(len, tile);
+      hp.seg_tile0[s] = static_cast<int32_t>(tiles);
+      hp.seg_pages[s] = static_cast<int32_t>(P);
+      hp.seg_kind[s] = is_query ? sift::kQuery : sift::kDocument;
+      hp.seg_first[s] = psp[b];
+      hp.seg_la_off[s] = static_cast<int32_t>(la_off);
+      hp.seg_ca_off[s] = static_cast<int32_t>(ca_off);
+      if (!is_query) {
+        la_off += hq * la_nbytes(P);
+        ca_off += hq * ca_nbytes(P);
+        if (la_off > i32max || ca_off > i32max) return SIFT_E_CAPACITY;
+      }
+      // causal tiles of rows i = 0..P-1 of this segment: (tiles - lo) + i + 1
+      dense += P * (tiles - lo) + P * (P + 1) / 2;
+      tiles += P;
+      if (tiles > i32max) return SIFT_E_CAPACITY;
+    }
+  }
+  hp.num_tiles = static_cast<int32_t>(tiles);
+  hp.la_bytes = la_off;
+  hp.ca_bytes = ca_off;
+  hp.dense_tiles = dense;
+  if (dense * hq >= i32max) return SIFT_E_CAPACITY;  // int32 list offsets
+  if (static_cast<int64_t>(tiles) * hq >= i32max) return SIFT_E_CAPACITY;
+
+  hp.tile_seg.resize(tiles);
+  hp.tile_tok0.resize(tiles);
+  hp.tile_len.resize(tiles);
+  hp.tile_lo.resize(tiles);
+  for (int32_t b = 0; b < B; ++b) {
+    const int32_t lo = hp.seg_tile0[psp[b]];
+    for (int32_t s = psp[b]; s < psp[b + 1]; ++s) {
+      for (int32_t i = 0; i < hp.seg_pages[s]; ++i) {
+        const int32_t m = hp.seg_tile0[s] + i;
+        hp.tile_seg[m] = s;
+        hp.tile_tok0[m] = so[s] + i * tile;
+        hp.tile_len[m] = std::min<int32_t>(tile, so[s + 1] - (so[s] + i * tile));
+        hp.tile_lo[m] = lo;
+      }
+    }
+  }
+
+  // Attention work units: (query head, M-blocks 2p and 2p+1 of a segment).
+  struct Pair {
+    int32_t m0, m1;
+    int64_t cost;  // causal tiles of the pair's later M-block: the list-length bound
+  };
+  std::vector<Pair> pairs;
+  for (int32_t s = 0; s < S; ++s) {
+    const int32_t lo = hp.seg_tile0[hp.seg_first[s]];  // first tile of the prompt
+    for (int32_t p = 0; p < hp.seg_pages[s]; p += 2) {
+      const int32_t m0 = hp.seg_tile0[s] + p;
+      const int32_t m1 = p + 1 < hp.seg_pages[s] ? m0 + 1 : -1;
+      pairs.push_back({m0, m1, (m1 >= 0 ? m1 : m0) - lo + 1});
+    }
+  }
+  // Units in locality order: kv head, then longest pair first, then the query
+  // heads of the group side by side (they read the same key tiles).
+  const int32_t g = hq / hkv;
+  std::vector<int32_t> pord(pairs.size());
+  std::iota(pord.begin(), pord.end(), 0);
+  std::stable_sort(pord.begin(), pord.end(),
+                   [&](int32_t x, int32_t y) { return pairs[x].cost > pairs[y].cost; });
+  const int64_t U = static_cast<int64_t>(pairs.size()) * hq;
+  if (U > i32max / 2) return SIFT_E_CAPACITY;
+  std::vector<int32_t> order;  // unit ids
+  order.reserve(U);
+  hp.unit_head.resize(U);
+  hp.unit_m0.resize(U);
+  hp.unit_m1.resize(U);
+  std::vector<int64_t> unit_cost(U);
+  int32_t u = 0;
+  for (int32_t kv = 0; kv < hkv; ++kv)
+    for (int32_t pi : pord)
+      for (int32_t j = 0; j < g; ++j) {
+        hp.unit_head[u] = kv * g + j;
+        hp.unit_m0[u] = pairs[pi].m0;
+        hp.unit_m1[u] = pairs[pi].m1;
+        unit_cost[u] = pairs[pi].cost;
+        order.push_back(u);
+        ++u;
+      }
+  // Split the locality order into kNumXcd contiguous chunks; workgroup
+  // x + kNumXcd * k runs chunk x's k-th unit (longest first inside a chunk).
+  std::vector<std::vector<int32_t>> chunk(kNumXcd);
+  int64_t longest = 0;
+  for (int x = 0; x < kNumXcd; ++x) {
+    const int64_t a = U * x / kNumXcd, z = U * (x + 1) / kNumXcd;
+    chunk[x].assign(order.begin() + a, order.begin() + z);
+    std::stable_sort(chunk[x].begin(), chunk[x].end(),
+                     [&](int32_t p, int32_t q) { return unit_cost[p] > unit_cost[q]; });
+    longest = std::max<int64_t>(longest, static_cast<int64_t>(chunk[x].size()));
+  }
+  hp.sched.assign(longest * kNumXcd, -1);
+  for (int x = 0; x < kNumXcd; ++x)
+    for (size_t k = 0; k < chunk[x].size(); ++k) hp.sched[x + kNumXcd * k] = chunk[x][k];
+  return SIFT_OK;
+}
+
+template <class T>
+size_t put(std::vector<uint8_t>& blob, const std::vector<T>& v) {
+  const size_t off = (blob.size() + 255) & ~size_t(255);
+  blob.resize(off + v.size() * sizeof(T));
+  if (!v.empty()) std::memcpy(blob.data() + off, v.data(), v.size() * sizeof(T));
+  return off;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sift_status_string(int32_t status) {
+  switch (status) {
+    case SIFT_OK: return "ok";
+    case SIFT_E_NULL: return "a required pointer is NULL";
+    case SIFT_E_SHAPE: return "tensor shapes do not match each other or the layout";
+    case SIFT_E_LAYOUT: return "malformed prompt layout";
+    case SIFT_E_UNSUPPORTED: return "tile size, head size or dtype not supported";
+    case SIFT_E_CAPACITY: return "a buffer or index range is too small";
+    case SIFT_E_HIP: return "a HIP runtime call failed";
+    case SIFT_E_PLAN: return "the plan does not match the arguments or the device";
+    default: return "unknown status";
+  }
+}
+
+sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
+                             int32_t num_kv_heads, int32_t head_dim, int32_t tile,
+                             sift_plan** plan_out) {
+  if (layout == nullptr || plan_out == nullptr) return SIFT_E_NULL;
+  *plan_out = nullptr;
+  if (num_q_heads < 1 || num_kv_heads < 1 || num_q_heads % num_kv_heads != 0) return SIFT_E_SHAPE;
+  if (head_dim != 64 && head_dim != 128) return SIFT_E_UNSUPPORTED;
+  if (tile != 16 && tile != 32 && tile != 64) return SIFT_E_UNSUPPORTED;
+  HostPlan hp;
+  sift_status st = build_host_plan(layout, num_q_heads, num_kv_heads, tile, hp);
+  if (st != SIFT_OK) return st;
+
+  std::vector<uint8_t> blob;
+  const size_t o_seg_tile0 = put(blob, hp.seg_tile0);
+  const size_t o_seg_pages = put(blob, hp.seg_pages);
+  const size_t o_seg_kind = put(blob, hp.seg_kind);
+  const size_t o_seg_first = put(blob, hp.seg_first);
+  const size_t o_seg_la = put(blob, hp.seg_la_off);
+  const size_t o_seg_ca = put(blob, hp.seg_ca_off);
+  const size_t o_tile_seg = put(blob, hp.tile_seg);
+  const size_t o_tile_tok0 = put(blob, hp.tile_tok0);
+  const size_t o_tile_len = put(blob, hp.tile_len);
+  const size_t o_tile_lo = put(blob, hp.tile_lo);
+  const size_t o_sched = put(blob, hp.sched);
+  const size_t o_uh = put(blob, hp.unit_head);
+  const size_t o_um0 = put(blob, hp.unit_m0);
+  const size_t o_um1 = put(blob, hp.unit_m1);
+  const int64_t rows = static_cast<int64_t>(hp.num_tiles) * num_q_heads;
+  const int64_t cap = hp.dense_tiles * num_q_heads;
+  const size_t o_counts = (blob.size() + 255) & ~size_t(255);
+  const size_t o_rowptr = (o_counts + rows * 4 + 255) & ~size_t(255);
+  const size_t o_col = (o_rowptr + (rows + 1) * 4 + 255) & ~size_t(255);
+  const size_t total = o_col + std::max<int64_t>(cap, 1) * 4;
+
+  sift_plan* plan = new (std::nothrow) sift_plan();
+  if (plan == nullptr) return SIFT_E_HIP;
+  if (hipGetDevice(&plan->device) != hipSuccess) {
+    delete plan;
+    return SIFT_E_HIP;
+  }
+  if (hipMalloc(&plan->dev, total) != hipSuccess) {
+    delete plan;
+    return SIFT_E_HIP;
+  }
+  plan->dev_bytes = total;
+  if (!blob.empty() &&
+      hipMemcpy(plan->dev, blob.data(), blob.size(), hipMemcpyHostToDevice) != hipSuccess) {
+    (void)hipFree(plan->dev);
+    delete plan;
+    return SIFT_E_HIP;
+  }
+  auto P = [plan](size_t off) {
+    return reinterpret_cast<int32_t*>(static_cast<uint8_t*>(plan->dev) + off);
+  };
+  plan->pt.seg_tile0 = P(o_seg_tile0);
+  plan->pt.seg_pages = P(o_seg_pages);
+  plan->pt.seg_kind = P(o_seg_kind);
+  plan->pt.seg_first = P(o_seg_first);
+  plan->pt.seg_la_off = P(o_seg_la);
+  plan->pt.seg_ca_off = P(o_seg_ca);
+  plan->pt.tile_seg = P(o_tile_seg);
+  plan->pt.tile_tok0 = P(o_tile_tok0);
+  plan->pt.tile_len = P(o_tile_len);
+  plan->pt.tile_lo = P(o_tile_lo);
+  plan->pt.num_tiles = hp.num_tiles;
+  plan->pt.num_q_heads = num_q_heads;
+  plan->wt.sched = P(o_sched);
+  plan->wt.unit_head = P(o_uh);
+  plan->wt.unit_m0 = P(o_um0);
+  plan->wt.unit_m1 = P(o_um1);
+  plan->wt.grid = static_cast<int32_t>(hp.sched.size());
+  plan->counts = P(o_counts);
+  plan->row_ptr = P(o_rowptr);
+  plan->col_idx = P(o_col);
+
+  sift_plan_info& in = plan->info;
+  in.num_tokens = hp.num_tokens;
+  in.num_segments = hp.num_segments;
+  in.num_tiles = hp.num_tiles;
+  in.num_q_heads = num_q_heads;
+  in.num_kv_heads = num_kv_heads;
+  in.head_dim = head_dim;
+  in.tile = tile;
+  in.num_work_units = static_cast<int32_t>(hp.unit_head.size());
+  in.num_rows = rows;
+  in.list_capacity = cap;
+  in.la_bytes = hp.la_bytes;
+  in.ca_bytes = hp.ca_bytes;
+  in.scratch_bytes = static_cast<int64_t>(total);
+  *plan_out = plan;
+  return SIFT_OK;
+}
+
+sift_status sift_plan_destroy(sift_plan* plan) {
+  if (plan == nullptr) return SIFT_OK;
+  sift_status st = SIFT_OK;
+  if (plan->dev != nullptr) {
+    if (hipDeviceSynchronize() != hipSuccess) st = SIFT_E_HIP;
+    if (hipFree(plan->dev) != hipSuccess) st = SIFT_E_HIP;
+  }
+  delete plan;
+  return st;
+}
+
+sift_status sift_plan_get_info(const sift_plan* plan, sift_plan_info* info) {
+  if (plan == nullptr || info == nullptr) return SIFT_E_NULL;
+  *info = plan->info;
+  return SIFT_OK;
+}
+
+sift_status sift_decode_tiles(sift_plan* plan, const uint8_t* local_bitmap,
+                              const uint8_t* cross_bitmap, int32_t* row_ptr, int32_t* col_idx,
+                              int64_t col_capacity, void* stream) {
+  if (plan == nullptr || row_ptr == nullptr) return SIFT_E_NULL;
+  if (plan->info.la_bytes > 0 && local_bitmap == nullptr) return SIFT_E_NULL;
+  if (plan->info.ca_bytes > 0 && cross_bitmap == nullptr) return SIFT_E_NULL;
+  if (plan->info.list_capacity > 0 && col_idx == nullptr) return SIFT_E_NULL;
+  if (col_capacity < plan->info.list_capacity) return SIFT_E_CAPACITY;
+  sift_status st = check_device(plan);
+  if (st != SIFT_OK) return st;
+  const hipError_t e = sift::launch_decode(plan->pt, local_bitmap, cross_bitmap, plan->counts,
+                                           row_ptr, col_idx, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SIFT_OK : SIFT_E_HIP;
+}
+
+sift_status sift_sparse_attention(sift_plan* plan, const sift_tensor* q, const sift_tensor* k,
+                                  const sift_tensor* v, const int32_t* row_ptr,
+                                  const int32_t* col_idx, int64_t col_capacity,
+                                  float softmax_scale, sift_tensor* out, void* stream) {
+  if (plan == nullptr || row_ptr == nullptr) return SIFT_E_NULL;
+  const sift_plan_info& in = plan->info;
+  sift_status st = check_io(q, k, v, out, in.num_tokens, in.num_q_heads, in.num_kv_heads,
+                            in.head_dim, in.tile);
+  if (st != SIFT_OK) return st;
+  if (col_capacity < 0) return SIFT_E_CAPACITY;
+  if (col_capacity > 0 && col_idx == nullptr) return SIFT_E_NULL;
+  const bool bf16 = q->dtype == SIFT_BF16;
+  if (!(softmax_scale > 0.f) || !std::isfinite(softmax_scale))
+    softmax_scale = 1.0f / std::sqrt(static_cast<float>(in.head_dim));
+  if ((st = check_device(plan)) != SIFT_OK) return st;
+  sift::AttnArgs a{};
+  a.q = q->data;
+  a.k = k->data;
+  a.v = v->data;
+  a.out = out->data;
+  a.row_ptr = row_ptr;
+  a.col_idx = col_idx;
+  a.col_capacity = col_capacity;
+  a.hq = in.num_q_heads;
+  a.hkv = in.num_kv_heads;
+  a.head_dim = in.head_dim;
+  a.tile = in.tile;
+  a.scale_log2 = softmax_scale * 1.4426950408889634f;
+  a.out_f32 = out->dtype == SIFT_F32 ? 1 : 0;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const hipError_t e = bf16 ? sift::launch_attn_bf16(plan->pt, plan->wt, a, s)
+                            : sift::launch_attn_f32(plan->pt, a, s);
+  return e == hipSuccess ? SIFT_OK : SIFT_E_HIP;
+}
+
+sift_status sift_plan_run(sift_plan* plan, const sift_tensor* q, const sift_tensor* k,
+                          const sift_tensor* v, const uint8_t* local_bitmap,
+                          const uint8_t* cross_bitmap, float softmax_scale, sift_tensor* out,
+                          void* stream) {
+  if (plan == nullptr) return SIFT_E_NULL;
+  const sift_plan_info& in = plan->info;
+  // check everything before enqueuing the decode
+  sift_status st = check_io(q, k, v, out, in.num_tokens, in.num_q_heads, in.num_kv_heads,
+                            in.head_dim, in.tile);
+  if (st != SIFT_OK) return st;
+  if (in.la_bytes > 0 && local_bitmap == nullptr) return SIFT_E_NULL;
+  if (in.ca_bytes > 0 && cross_bitmap == nullptr) return SIFT_E_NULL;
+  st = sift_decode_tiles(plan, local_bitmap, cross_bitmap, plan->row_ptr, plan->col_idx,
+                         in.list_capacity, stream);
+  if (st != SIFT_OK) return st;
+  return sift_sparse_attention(plan, q, k, v, plan->row_ptr, plan->col_idx, in.list_capacity,
+                               softmax_scale, out, stream);
+}
+
+sift_status sift_sparse_prefill(const sift_tensor* q, const sift_tensor* k, const sift_tensor* v,
+                                const sift_layout* doc_offsets, const uint8_t* local_bitmap,
+                                const uint8_t* cross_bitmap, int32_t tile, sift_tensor* out,
+                                void* stream) {
+  if (q == nullptr || k == nullptr || v == nullptr || out == nullptr || doc_offsets == nullptr)
+    return SIFT_E_NULL;
+  // validate layout, shapes and bitmaps on the host before touching the device
+  {
+    if (q->heads < 1 || k->heads < 1 || q->heads % k->heads != 0) return SIFT_E_SHAPE;
+    if (q->head_dim != 64 && q->head_dim != 128) return SIFT_E_UNSUPPORTED;
+    if (tile != 16 && tile != 32 && tile != 64) return SIFT_E_UNSUPPORTED;
+    HostPlan hp;
+    sift_status st0 = build_host_plan(doc_offsets, q->heads, k->heads, tile, hp);
+    if (st0 != SIFT_OK) return st0;
+    st0 = check_io(q, k, v, out, hp.num_tokens, q->heads, k->heads, q->head_dim, tile);
+    if (st0 != SIFT_OK) return st0;
+    if (hp.la_bytes > 0 && local_bitmap == nullptr) return SIFT_E_NULL;
+    if (hp.ca_bytes > 0 && cross_bitmap == nullptr) return SIFT_E_NULL;
+  }
+  sift_plan* plan = nullptr;
+  sift_status st = sift_plan_create(doc_offsets, q->heads, k->heads, q->head_dim, tile, &plan);
+  if (st != SIFT_OK) return st;
+  st = sift_plan_run(plan, q, k, v, local_bitmap, cross_bitmap, 0.f, out, stream);
+  if (st == SIFT_OK && hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess)
+    st = SIFT_E_HIP;
+  const sift_status st2 = sift_plan_destroy(plan);
+  return st != SIFT_OK ? st : st2;
+}
+
+}  // extern "C"

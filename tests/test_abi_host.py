@@ -1,0 +1,79 @@
+"""Host-side checks of libsift that need no GPU: the library loads, exports
+every function include/sift.h declares, and rejects malformed arguments on
+the host before touching the device."""
+
+import ctypes
+
+import numpy as np
+import pytest
+
+from paper_2606_09441_amd import _lib as B
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    L = B.lib()
+    names = B.header_functions()
+    assert "sift_sparse_prefill" in names and "sift_decode_tiles" in names
+    assert len(names) == 8
+    for n in names:
+        assert hasattr(L, n), n
+    # the binding declares every one of them too
+    assert set(names) == set(B._SIGS)
+
+
+def test_status_strings():
+    L = B.lib()
+    for code in range(8):
+        assert L.sift_status_string(code)
+    assert L.sift_status_string(99) == b"unknown status"
+
+
+def _t(tokens, heads, dim, dtype=B.SIFT_BF16, data=1):
+    return B.SiftTensor(data, dtype, tokens, heads, dim)
+
+
+def _prefill(q, k, v, so, ps, tile=64, la=1, ca=1, out=None):
+    lay, keep = B.layout_struct(so, ps)
+    out = out if out is not None else _t(q.tokens, q.heads, q.head_dim, q.dtype)
+    return B.lib().sift_sparse_prefill(ctypes.byref(q), ctypes.byref(k), ctypes.byref(v), ctypes.byref(lay),
+                                       ctypes.c_void_p(la), ctypes.c_void_p(ca), tile,
+                                       ctypes.byref(out), None)
+
+
+def test_prefill_rejects_bad_arguments_on_the_host():
+    so, ps = [0, 64, 128, 160], [0, 3]
+    q, k = _t(160, 4, 128), _t(160, 2, 128)
+    # shapes
+    assert _prefill(_t(161, 4, 128), k, k, so, ps) == 2                 # tokens differ from layout
+    assert _prefill(q, _t(160, 3, 128), _t(160, 3, 128), so, ps) == 2   # Hq % Hkv != 0
+    assert _prefill(q, k, _t(160, 2, 64), so, ps) == 2                  # head dims differ
+    # layouts
+    assert _prefill(q, k, k, [0, 0, 128, 160], ps) == 3                 # empty document
+    assert _prefill(q, k, k, [0, 64, 32, 160], ps) == 3                 # offsets go back
+    assert _prefill(q, k, k, so, [1, 3]) == 3                           # prompt_seg_ptr[0] != 0
+    # unsupported
+    assert _prefill(q, k, k, so, ps, tile=48) == 4
+    assert _prefill(_t(160, 4, 96), _t(160, 2, 96), _t(160, 2, 96), so, ps) == 4
+    assert _prefill(q, k, k, so, ps, tile=16) == 4                      # bf16 MFMA path needs T = 64
+    q32 = _t(160, 4, 128, B.SIFT_F32)
+    assert _prefill(q32, _t(160, 2, 128, B.SIFT_F32), _t(160, 2, 128, B.SIFT_F32), so, ps,
+                    out=_t(160, 4, 128, B.SIFT_BF16)) == 4             # fp32 in, bf16 out
+    assert _prefill(q, _t(160, 2, 128, B.SIFT_F32), k, so, ps) == 4     # mixed input dtypes
+    # nulls
+    assert _prefill(q, k, k, so, ps, la=0) == 1
+    assert _prefill(q, k, k, so, ps, ca=0) == 1
+    assert _prefill(_t(160, 4, 128, data=0), k, k, so, ps) == 1
+    assert B.lib().sift_sparse_prefill(None, None, None, None, None, None, 64, None, None) == 1
+
+
+def test_plan_create_rejects_bad_layouts_on_the_host():
+    h = ctypes.c_void_p()
+    for so, ps, code in [([0, 0, 10], [0, 2], 3), ([0, 5], [0, 0], 3), ([1, 5], [0, 1], 3)]:
+        lay, keep = B.layout_struct(so, ps)
+        assert B.lib().sift_plan_create(ctypes.byref(lay), 4, 2, 128, 64, ctypes.byref(h)) == code
+    lay, keep = B.layout_struct([0, 64, 70], [0, 2])
+    assert B.lib().sift_plan_create(ctypes.byref(lay), 4, 3, 128, 64, ctypes.byref(h)) == 2
+    assert B.lib().sift_plan_create(ctypes.byref(lay), 4, 2, 128, 8, ctypes.byref(h)) == 4
+    assert B.lib().sift_plan_create(ctypes.byref(lay), 4, 2, 80, 64, ctypes.byref(h)) == 4
+    assert B.lib().sift_plan_create(None, 4, 2, 128, 64, ctypes.byref(h)) == 1
+    assert B.lib().sift_plan_destroy(None) == 0
