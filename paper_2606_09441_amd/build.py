@@ -22,6 +22,10 @@ LIB_PATH = os.path.join(HERE, "libsift.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
 SOURCES = ["decode.hip", "attn_bf16.hip", "attn_f32.hip", "sift_api.cpp"]
+# Per-source extra flags.  The bf16 attention kernel takes row maxima of MFMA
+# results that are finite or -inf (masked): NaN canonicalisation around
+# fmaxf would only add instructions, so NaNs are not honoured there.
+EXTRA = {"attn_bf16.hip": ["-fno-honor-nans"]}
 
 ARCH = "gfx950"
 COMMON = [
@@ -45,7 +49,7 @@ def _hipcc() -> str:
 
 def _compile(src: str, hipcc: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [hipcc, *COMMON]
+    cmd = [hipcc, *COMMON, *EXTRA.get(src, [])]
     if src.endswith(".cpp"):
         cmd += ["-x", "hip"]
     cmd += ["-c", os.path.join(CSRC, src), "-o", obj]

@@ -16,9 +16,16 @@
 //    and row max / row sum are in-lane plus one exchange with lane ^ 32.
 //  * The S^T accumulator, rounded to bf16, is already the B operand of
 //    O^T += V^T P^T (same MFMA): the 16 keys of a k-step are permuted inside
-//    the step, and V^T is written to LDS in that permuted key order.
-//  * K rows are staged row-major (padded pitch), V transposed on the way in
-//    (registers -> LDS), double buffered: the global loads of tile t+1 are in
+//    the step (lane half hf holds keys 4hf..4hf+3 and 8+4hf..8+4hf+3), and
+//    the V^T A operand is read in that order from row-major V with gfx950's
+//    LDS transpose read (ds_read_b64_tr_b16: in a 16-lane group, lane i gets
+//    element i%4 of the 64-bit chunk addressed by lane 4j + i/4, j = 0..3,
+//    i.e. column i of a 4-row block when lane 4j+q addresses row j, columns
+//    4q..4q+3).
+//  * K and V tiles are staged row-major in LDS with padded pitches (K: 272 B,
+//    conflict-free 16 B row reads; V: 320 B, so the 4 rows x 64 B that two
+//    16-lane groups of a transpose read touch fall on disjoint banks), double
+//    buffered: the global loads of tile t+1 are in
 //    flight while tile t is computed; one barrier per tile.
 //  * Online softmax in the log2 domain; P is rounded to bf16 and the row sum
 //    adds exactly those rounded values (v_dot2_f32_bf16 against 1.0), so
@@ -39,14 +46,16 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
 constexpr int kT = 64;
 constexpr int kD = 128;
 constexpr int kKPitch = kD + 8;            // bf16 per K row in LDS (272 B)
-constexpr int kVPitch = kT + 8;            // bf16 per V^T row in LDS (144 B)
+constexpr int kVPitch = kD + 32;           // bf16 per V row in LDS (320 B)
 constexpr int kKElems = kT * kKPitch;
-constexpr int kVElems = kD * kVPitch;
-constexpr int kStage = kKElems + kVElems;  // one buffer: 35840 B
+constexpr int kVElems = kT * kVPitch;
+constexpr int kStage = kKElems + kVElems;  // one buffer: 37888 B
 constexpr int kNone = 0x7fffffff;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 x) { return __builtin_bit_cast(bf16x8, x); }
@@ -84,72 +93,71 @@ __device__ __forceinline__ Step next_step(ListCursor& a, ListCursor& b) {
   return s;
 }
 
-// Global -> register staging of one K/V tile (256 threads).
-//   K: thread t loads rows it*16 + t/16 (it = 0..3), 16 B chunk t%16.
-//   V: thread t loads, for key group G = t/32 and head-dim quad dq = t%32,
-//      the 8 keys base(G) + {0,1,2,3,8,9,10,11} at dims 4dq..4dq+3, with
-//      base(G) = 32(G>>2) + 16((G>>1)&1) + 4(G&1).
+// Global -> register staging of one K/V tile (256 threads): thread t loads
+// rows it*16 + t/16 (it = 0..3), 16 B chunk t%16, of K and of V.
+// Loads are buffer loads through a per-tile resource whose base is the
+// tile's first token and whose range ends with the tile's last valid row:
+// rows past the end of a partial tile read as zero, with no branch.  The
+// per-thread byte offset is fixed for the whole kernel; the row block is a
+// scalar offset.
 struct TileRegs {
   u32x4 k[4];
-  u32x2 v[8];
+  u32x4 v[4];
 };
 
+constexpr int kBufferWord3 = 0x00020000;  // gfx9-family raw buffer resource word 3
+
 __device__ __forceinline__ void load_tile(TileRegs& r, const __bf16* __restrict__ kp,
-                                          const __bf16* __restrict__ vp, int tok0, int len,
-                                          int hkv, int kvh, int tid) {
+                                          const __bf16* __restrict__ vp, int64_t tile_base,
+                                          int len, int kstride, int off) {
+  const int row_bytes = kstride * 2;
+  const int valid = (len - 1) * row_bytes + kD * 2;  // through the last valid row
+  const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<__bf16*>(kp + tile_base), 0, valid, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<__bf16*>(vp + tile_base), 0, valid, kBufferWord3);
 #pragma unroll
   for (int it = 0; it < 4; ++it) {
-    const int row = it * 16 + (tid >> 4);
-    const int ch = tid & 15;
-    if (row < len) {
-      const __bf16* src = kp + (static_cast<int64_t>(tok0 + row) * hkv + kvh) * kD + ch * 8;
-      r.k[it] = *reinterpret_cast<const u32x4*>(src);
-    } else {
-      r.k[it] = u32x4{0u, 0u, 0u, 0u};
-    }
-  }
-  const int G = tid >> 5;
-  const int dq = tid & 31;
-  const int base = 32 * (G >> 2) + 16 * ((G >> 1) & 1) + 4 * (G & 1);
-#pragma unroll
-  for (int t = 0; t < 8; ++t) {
-    const int key = base + (t < 4 ? t : t + 4);
-    if (key < len) {
-      const __bf16* src = vp + (static_cast<int64_t>(tok0 + key) * hkv + kvh) * kD + dq * 4;
-      r.v[t] = *reinterpret_cast<const u32x2*>(src);
-    } else {
-      r.v[t] = u32x2{0u, 0u};
-    }
+    r.k[it] = __builtin_bit_cast(
+        u32x4, __builtin_amdgcn_raw_buffer_load_b128(kr, off, it * 16 * row_bytes, 0));
+    r.v[it] = __builtin_bit_cast(
+        u32x4, __builtin_amdgcn_raw_buffer_load_b128(vr, off, it * 16 * row_bytes, 0));
   }
 }
 
-// Register -> LDS: K row-major; V transposed to V^T[d][pos] with the key at
-// pos = key with bits 2 and 3 swapped (the permutation the P^T operand uses).
+// Register -> LDS, both row-major (16 consecutive lanes write one 256 B row).
 __device__ __forceinline__ void store_tile(const TileRegs& r, __bf16* stage, int tid) {
   __bf16* Ks = stage;
-  __bf16* Vt = stage + kKElems;
+  __bf16* Vs = stage + kKElems;
+  const int row = tid >> 4;
+  const int ch = (tid & 15) * 8;
 #pragma unroll
   for (int it = 0; it < 4; ++it) {
-    const int row = it * 16 + (tid >> 4);
-    const int ch = tid & 15;
-    *reinterpret_cast<u32x4*>(Ks + row * kKPitch + ch * 8) = r.k[it];
-  }
-  const int G = tid >> 5;
-  const int dq = tid & 31;
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    // element e (dim 4dq+e) of each of the 8 loaded keys, packed in key order
-    const int w = e >> 1;
-    u32x4 o;
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const unsigned lo = r.v[2 * p][w];
-      const unsigned hi = r.v[2 * p + 1][w];
-      o[p] = (e & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
-    }
-    *reinterpret_cast<u32x4*>(Vt + (4 * dq + e) * kVPitch + G * 8) = o;
+    *reinterpret_cast<u32x4*>(Ks + (it * 16 + row) * kKPitch + ch) = r.k[it];
+    *reinterpret_cast<u32x4*>(Vs + (it * 16 + row) * kVPitch + ch) = r.v[it];
   }
 }
+
+// A operand of O^T += V^T P^T for head-dim block db and key step st: lane l
+// (l32 = l & 31, hf = l >> 5) needs V[key][32db + l32] for the 8 keys
+// 16st + 4hf + {0,1,2,3} and 16st + 8 + 4hf + {0,1,2,3}: two transpose reads
+// of 4-row blocks.  vaddr is this lane's source address for db = st = 0 and
+// the first block: row ((l & 15) >> 2) + 4hf, columns 16((l >> 4) & 1) + 4(l & 3).
+__device__ __forceinline__ bf16x8 v_operand(const __bf16* vaddr, int db, int st) {
+  const __bf16* p0 = vaddr + (16 * st) * kVPitch + 32 * db;
+  const __bf16* p1 = p0 + 8 * kVPitch;
+  const bf16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      (lds_bf16x4*)((__attribute__((address_space(3))) __bf16*)p0));
+  const bf16x4 y = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      (lds_bf16x4*)((__attribute__((address_space(3))) __bf16*)p1));
+  return bf16x8{x[0], x[1], x[2], x[3], y[0], y[1], y[2], y[3]};
+}
+
+// Scores are compared against the running reference max only in steps of
+// kLazy (log2 units): the reference moves, and O and l are rescaled, only
+// when a tile's max exceeds it by more than kLazy.  exp2 arguments stay
+// <= kLazy, so P <= 2^kLazy: no overflow, and the same bf16 relative precision.
+constexpr float kLazy = 8.0f;
 
 template <bool kOutF32>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTables wt,
@@ -163,18 +171,21 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
   const int m1 = wt.unit_m1[unit];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int l32 = lane & 31;
   const int hf = lane >> 5;
   const int hq = a.hq;
   const int hkv = a.hkv;
   const int kvh = h / (hq / hkv);
+  const int kstride = hkv * kD;
   const int lo = pt.tile_lo[m0];
   const int mine = wave < 2 ? m0 : m1;     // this wavefront's M-block (-1: none)
   const int qrow = (wave & 1) * 32 + l32;  // query row inside that M-block
   const __bf16* __restrict__ qp = static_cast<const __bf16*>(a.q);
   const __bf16* __restrict__ kp = static_cast<const __bf16*>(a.k);
   const __bf16* __restrict__ vp = static_cast<const __bf16*>(a.v);
+
+  const int off = ((tid >> 4) * kstride + (tid & 15) * 8) * 2;  // bytes
 
   // Q^T fragments (B operand of S^T = K Q^T): lane holds query row qrow,
   // dims 16s + 8hf .. +7 for k-step s.
@@ -203,12 +214,12 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
   ListCursor lb{a.col_idx, 0, 0, lo, m1};
   {
     const int64_t r0 = static_cast<int64_t>(h) * M + m0;
-    la.i = clampi(a.row_ptr[r0]);
-    la.e = max(la.i, clampi(a.row_ptr[r0 + 1]));
+    la.i = clampi(__builtin_amdgcn_readfirstlane(a.row_ptr[r0]));
+    la.e = max(la.i, clampi(__builtin_amdgcn_readfirstlane(a.row_ptr[r0 + 1])));
     if (m1 >= 0) {
       const int64_t r1 = static_cast<int64_t>(h) * M + m1;
-      lb.i = clampi(a.row_ptr[r1]);
-      lb.e = max(lb.i, clampi(a.row_ptr[r1 + 1]));
+      lb.i = clampi(__builtin_amdgcn_readfirstlane(a.row_ptr[r1]));
+      lb.e = max(lb.i, clampi(__builtin_amdgcn_readfirstlane(a.row_ptr[r1 + 1])));
     }
   }
 
@@ -217,99 +228,113 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
   for (int db = 0; db < 4; ++db)
 #pragma unroll
     for (int v = 0; v < 16; ++v) o[db][v] = 0.f;
-  float mrun = -INFINITY;
-  float lrun = 0.f;
+  float mref = -INFINITY;  // reference max, already multiplied by c
+  float lrun = 0.f;        // this lane's share of the row sum (its 32 keys per tile)
   const float c = a.scale_log2;
 
   TileRegs regs;
   Step cur = next_step(la, lb);
   if (cur.n != kNone) {
-    load_tile(regs, kp, vp, pt.tile_tok0[cur.n], pt.tile_len[cur.n], hkv, kvh, tid);
+    load_tile(regs, kp, vp, (static_cast<int64_t>(pt.tile_tok0[cur.n]) * hkv + kvh) * kD,
+              pt.tile_len[cur.n], kstride, off);
     store_tile(regs, lds, tid);
   }
   __syncthreads();
   int buf = 0;
   while (cur.n != kNone) {
     const Step nxt = next_step(la, lb);
-    if (nxt.n != kNone)
-      load_tile(regs, kp, vp, pt.tile_tok0[nxt.n], pt.tile_len[nxt.n], hkv, kvh, tid);
+    // Prefetch the next tile (on the last step: the current one again, so
+    // that loads and LDS stores are unconditional and no wait for them is
+    // placed before this step's compute).
+    const int pf = nxt.n != kNone ? nxt.n : cur.n;
+    load_tile(regs, kp, vp, (static_cast<int64_t>(pt.tile_tok0[pf]) * hkv + kvh) * kD,
+              pt.tile_len[pf], kstride, off);
 
     const bool part = wave < 2 ? cur.in0 : cur.in1;
     if (part) {
       const __bf16* Ks = lds + buf * kStage;
-      const __bf16* Vt = Ks + kKElems;
-      // ---- S^T = K Q^T: two 32-key blocks
-      f32x16 sacc[2];
+      const __bf16* vaddr = Ks + kKElems + (((lane & 15) >> 2) + 4 * hf) * kVPitch +
+                            16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+      // ---- S^T = K Q^T: two independent 32-key chains, interleaved
+      f32x16 s0, s1;
+      {
+        const __bf16* k0 = Ks + l32 * kKPitch + 8 * hf;
+        const __bf16* k1 = k0 + 32 * kKPitch;
+        bf16x8 a0 = as_bf16x8(*reinterpret_cast<const u32x4*>(k0));
+        bf16x8 a1 = as_bf16x8(*reinterpret_cast<const u32x4*>(k1));
+        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[0], f32x16{}, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[0], f32x16{}, 0, 0, 0);
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) sacc[kb][v] = 0.f;
-        const __bf16* krow = Ks + (32 * kb + l32) * kKPitch + 8 * hf;
-#pragma unroll
-        for (int s = 0; s < 8; ++s) {
-          const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(krow + 16 * s));
-          sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc[kb], 0, 0, 0);
+        for (int s = 1; s < 8; ++s) {
+          a0 = as_bf16x8(*reinterpret_cast<const u32x4*>(k0 + 16 * s));
+          a1 = as_bf16x8(*reinterpret_cast<const u32x4*>(k1 + 16 * s));
+          s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[s], s0, 0, 0, 0);
+          s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[s], s1, 0, 0, 0);
         }
       }
-      // ---- causal mask on the diagonal tile, length mask on a partial tile
+      // ---- causal mask on the diagonal tile, length mask on a partial tile.
+      // Key of value v of block kb: 32kb + 8(v>>2) + 4hf + (v&3); the
+      // constant part is compared against limits shifted by 4hf.
       const int klen = pt.tile_len[cur.n];
       if (cur.n == mine || klen < kT) {
-        const bool diag = cur.n == mine;
+        const int klim = klen - 4 * hf;
+        const int qlim = cur.n == mine ? qrow - 4 * hf : 1 << 20;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int key = 32 * kb + 8 * (v >> 2) + 4 * hf + (v & 3);
-            if (key >= klen || (diag && key > qrow)) sacc[kb][v] = -INFINITY;
-          }
+        for (int v = 0; v < 16; ++v) {
+          const int kc = 8 * (v >> 2) + (v & 3);
+          if (kc >= klim || kc > qlim) s0[v] = -INFINITY;
+          if (kc + 32 >= klim || kc + 32 > qlim) s1[v] = -INFINITY;
+        }
       }
-      // ---- online softmax (log2 domain)
-      float mx = sacc[0][0];
+      // ---- online softmax in the log2 domain, lazy reference max
+      float mx = fmaxf(s0[0], s1[0]);
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[kb][v]);
+      for (int v = 1; v < 16; ++v) mx = fmaxf(mx, fmaxf(s0[v], s1[v]));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mnew = fmaxf(mrun, mx);
-      const float mc = mnew == -INFINITY ? 0.f : mnew * c;
-      const float alpha = __builtin_amdgcn_exp2f(mrun * c - mc);
-      mrun = mnew;
+      const float mxs = mx * c;
+      const bool grow = mxs > mref + kLazy;
+      if (__builtin_amdgcn_ballot_w64(grow)) {
+        const float mnew = grow ? mxs : mref;
+        const float alpha = __builtin_amdgcn_exp2f(mref - mnew);
+        mref = mnew;
+        lrun *= alpha;
+#pragma unroll
+        for (int db = 0; db < 4; ++db)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
+      }
+      const float base = mref == -INFINITY ? 0.f : mref;
       bf16x8 pb[4];
       float psum = 0.f;
+      const bf16x2 ones = bf16x2{static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
 #pragma unroll
       for (int st = 0; st < 4; ++st) {
-        const int kb = st >> 1;
         const int v0 = 8 * (st & 1);
 #pragma unroll
         for (int t = 0; t < 8; t += 2) {
-          const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[kb][v0 + t], c, -mc));
-          const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[kb][v0 + t + 1], c, -mc));
+          const float x0 = (st < 2) ? s0[v0 + t] : s1[v0 + t];
+          const float x1 = (st < 2) ? s0[v0 + t + 1] : s1[v0 + t + 1];
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(x0, c, -base));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(x1, c, -base));
           const bf16x2 pp = bf16x2{static_cast<__bf16>(p0), static_cast<__bf16>(p1)};
           pb[st][t] = pp[0];
           pb[st][t + 1] = pp[1];
-          psum = __builtin_amdgcn_fdot2_f32_bf16(pp, bf16x2{static_cast<__bf16>(1.f),
-                                                            static_cast<__bf16>(1.f)},
-                                                 psum, false);
+          psum = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, psum, false);
         }
       }
-      lrun = lrun * alpha + psum;
+      lrun += psum;
+      // ---- O^T += V^T P^T: four independent chains over the head dim
 #pragma unroll
-      for (int db = 0; db < 4; ++db)
+      for (int st = 0; st < 4; ++st) {
 #pragma unroll
-        for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
-      // ---- O^T += V^T P^T
-#pragma unroll
-      for (int db = 0; db < 4; ++db) {
-        const __bf16* vrow = Vt + (32 * db + l32) * kVPitch + 8 * hf;
-#pragma unroll
-        for (int st = 0; st < 4; ++st) {
-          const bf16x8 vf = as_bf16x8(*reinterpret_cast<const u32x4*>(vrow + 16 * st));
+        for (int db = 0; db < 4; ++db) {
+          const bf16x8 vf = v_operand(vaddr, db, st);
           o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[st], o[db], 0, 0, 0);
         }
       }
     }
 
-    if (nxt.n != kNone) store_tile(regs, lds + (buf ^ 1) * kStage, tid);
+    store_tile(regs, lds + (buf ^ 1) * kStage, tid);
     __syncthreads();
     buf ^= 1;
     cur = nxt;
