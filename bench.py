@@ -153,8 +153,11 @@ def main():
     flops = useful_flops(rp, ci, tlen, M, wl.d)
     nnz = int(rp[-1])
     density = nnz / plan.info["list_capacity"]
-    ms_decode = per_launch(lambda: plan.decode(la, ca, rp_t, ci_t), args.steps)
-    ms_attn = per_launch(lambda: plan.attention(q, k, v, rp_t, ci_t, out=out), args.steps)
+    # the two kernels of the path, each timed alone: decode (Section 5.1) and
+    # attention over the decoded lists (Section 5.2)
+    ms_decode = per_launch(lambda: plan.decode_internal(la, ca), args.steps)
+    plan.decode_internal(la, ca)
+    ms_attn = per_launch(lambda: plan.attention_internal(q, k, v, out=out), args.steps)
     log(f"decode {ms_decode * 1e3:.1f} us, attention {ms_attn:.3f} ms, nnz {nnz}, "
         f"density {density:.4f}, useful {flops / 1e12:.3f} TFLOP")
 
@@ -168,7 +171,8 @@ def main():
             step_d()
         ms_step_d = timed(step_d, max(2, args.steps // 2))
         rpd, cid = plan.decode(la_d, ca_d)
-        ms_attn_d = per_launch(lambda: plan.attention(q, k, v, rpd, cid, out=out),
+        plan.decode_internal(la_d, ca_d)
+        ms_attn_d = per_launch(lambda: plan.attention_internal(q, k, v, out=out),
                                max(2, args.steps // 2))
         torch.cuda.synchronize()
         rpd_h = rpd.cpu().numpy().astype(np.int64)

@@ -148,12 +148,31 @@ sift_status sift_plan_get_info(const sift_plan* plan, sift_plan_info* info);
  *   col_idx      device int32 [col_capacity], written: entries 0 .. nnz-1
  *   col_capacity must be >= the plan's list_capacity (an upper bound of nnz
  *                known on the host), else SIFT_E_CAPACITY.
- * Uses the plan's scratch for the counts.
+ * Uses the plan's scratch for the counts, and also leaves there the per-unit
+ * merged step lists (see sift_plan_attention).
  */
 sift_status sift_decode_tiles(sift_plan* plan, const uint8_t* local_bitmap,
                               const uint8_t* cross_bitmap, int32_t* row_ptr,
                               int32_t* col_idx, int64_t col_capacity,
                               void* stream);
+
+/*
+ * Decoding into the plan's own scratch (the lists and the per-unit merged
+ * step lists the bf16 attention kernel walks), as the first step of
+ * sift_plan_run.  Same bitmaps and errors as sift_decode_tiles.
+ */
+sift_status sift_plan_decode(sift_plan* plan, const uint8_t* local_bitmap,
+                             const uint8_t* cross_bitmap, void* stream);
+
+/*
+ * Sparse attention (Section 5.2) over the lists the last sift_plan_decode
+ * (or sift_plan_run, or sift_decode_tiles) on this plan produced: the
+ * second step of sift_plan_run.  Tensors, scale and output as in
+ * sift_sparse_attention.
+ */
+sift_status sift_plan_attention(sift_plan* plan, const sift_tensor* q, const sift_tensor* k,
+                                const sift_tensor* v, float softmax_scale, sift_tensor* out,
+                                void* stream);
 
 /*
  * Sparse attention (Section 5.2) over given lists: for every (h, M-block m),
@@ -165,6 +184,8 @@ sift_status sift_decode_tiles(sift_plan* plan, const uint8_t* local_bitmap,
  *                col_capacity entries of col_idx readable.  Entries outside
  *                the M-block's prompt or after the M-block are skipped;
  *                lists must be ascending.  A row whose list is empty gets 0.
+ *                (bf16 inputs: the lists are first merged into the plan's
+ *                per-unit step scratch.)
  *   softmax_scale  <= 0 selects 1/sqrt(D)
  *   out          device tensor [tokens][Hq][D], SIFT_BF16 or SIFT_F32 for
  *                bf16 inputs, SIFT_F32 for fp32 inputs.

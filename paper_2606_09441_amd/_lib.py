@@ -62,6 +62,10 @@ _SIGS = {
     "sift_sparse_attention": (ctypes.c_int, [_P, ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftTensor),
                                              ctypes.POINTER(SiftTensor), _P, _P, ctypes.c_int64,
                                              ctypes.c_float, ctypes.POINTER(SiftTensor), _P]),
+    "sift_plan_decode": (ctypes.c_int, [_P, _P, _P, _P]),
+    "sift_plan_attention": (ctypes.c_int, [_P, ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftTensor),
+                                           ctypes.POINTER(SiftTensor), ctypes.c_float,
+                                           ctypes.POINTER(SiftTensor), _P]),
     "sift_plan_run": (ctypes.c_int, [_P, ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftTensor),
                                      ctypes.POINTER(SiftTensor), _P, _P, ctypes.c_float,
                                      ctypes.POINTER(SiftTensor), _P]),
@@ -201,6 +205,22 @@ class Plan:
             self._h, ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), _ptr(row_ptr),
             _ptr(col_idx), col_idx.numel(), ctypes.c_float(0.0 if scale is None else scale),
             ctypes.byref(od), _stream_ptr(stream)))
+        return out
+
+    def decode_internal(self, la, ca, stream=None):
+        """Decode into the plan's own scratch (sift_plan_decode)."""
+        check("sift_plan_decode", lib().sift_plan_decode(self._h, _ptr(la), _ptr(ca),
+                                                         _stream_ptr(stream)))
+
+    def attention_internal(self, q, k, v, scale=None, out=None, out_dtype=None, stream=None):
+        """Attention over the plan's last decode (sift_plan_attention)."""
+        torch = _torch()
+        if out is None:
+            out = torch.empty(q.shape, dtype=out_dtype or q.dtype, device=q.device)
+        qd, kd, vd, od = tensor_desc(q), tensor_desc(k), tensor_desc(v), tensor_desc(out)
+        check("sift_plan_attention", lib().sift_plan_attention(
+            self._h, ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd),
+            ctypes.c_float(0.0 if scale is None else scale), ctypes.byref(od), _stream_ptr(stream)))
         return out
 
     def run(self, q, k, v, la, ca, scale=None, out=None, out_dtype=None, stream=None):

@@ -11,11 +11,15 @@
 //                 tile of the prompt up to the row's own (Section 5.1: query
 //                 M-blocks count all causal N-blocks).
 //   decode_scan   exclusive prefix sum of the counts -> row_ptr (one block).
-//   decode_write  one wavefront per row: CA pages of the earlier documents in
-//                 document order, then LA tiles j < i, then the diagonal;
-//                 each chunk of 64 bits is turned into indices with a ballot
-//                 and a lane-prefix popcount, so the output is dense and in
-//                 ascending global tile order.
+//   decode_write  one wavefront per attention work unit (query head, M-blocks
+//                 m0 and m0+1 of one segment): CA pages of the earlier
+//                 documents in document order, then LA tiles, then the
+//                 diagonals; each chunk of 64 bits becomes indices through a
+//                 ballot and a lane-prefix popcount, so every output is dense
+//                 and in ascending global tile order.  It writes both rows'
+//                 lists and the unit's merged step list (the union of the two
+//                 lists, each step flagged with the M-blocks that list it),
+//                 which the attention kernel streams.
 // Bits are most significant first inside each byte (Section 4.1).
 
 #include "sift_internal.h"
@@ -107,55 +111,152 @@ __global__ __launch_bounds__(1024) void decode_scan(const int32_t* __restrict__ 
   if (t == 1023) row_ptr[n] = excl;
 }
 
-// Append to col_idx[pos..] the indices base + b of the set bits among bits
-// b0 .. b0+n-1 of v, in bit order; returns the new pos.  Wave-cooperative.
-__device__ __forceinline__ int32_t emit_bits(const uint8_t* v, int b0, int n, int32_t base,
-                                             int32_t pos, int lane, int32_t* __restrict__ col) {
-  const unsigned long long below = (1ull << lane) - 1ull;
-  for (int c0 = 0; c0 < n; c0 += 64) {
-    const int b = c0 + lane;
-    const bool on = b < n && get_bit(v, b0 + b);
-    const unsigned long long mask = __ballot(on);
-    if (on) col[pos + __popcll(mask & below)] = base + b;
-    pos += __popcll(mask);
-  }
-  return pos;
-}
+// Wave-cooperative emitter of one unit's outputs.  Each call handles up to 64
+// candidate key tiles n (one per lane): `a` marks those m0 lists, `b` those
+// m1 lists; they are appended, in lane order, to m0's list, m1's list and the
+// merged step list.
+struct Emitter {
+  int32_t* col;
+  int2* steps;
+  const PlanTables* pt;
+  int32_t p0, p1, ps;  // next write positions (m0 list, m1 list, steps)
+  int32_t m0, m1;
+  int lane;
+  unsigned long long below;
 
-__global__ __launch_bounds__(256) void decode_write(PlanTables pt, const uint8_t* __restrict__ la,
+  __device__ __forceinline__ void emit(bool a, bool b, int32_t n) {
+    const unsigned long long ma = __ballot(a);
+    const unsigned long long mb = __ballot(b);
+    const unsigned long long mu = __ballot(a || b);
+    if (a) col[p0 + __popcll(ma & below)] = n;
+    if (b) col[p1 + __popcll(mb & below)] = n;
+    if (a || b) {
+      const int info = pt->tile_len[n] | (a ? kStepIn0 : 0) | (b ? kStepIn1 : 0) |
+                       (n == m0 ? kStepDiag0 : 0) | (n == m1 ? kStepDiag1 : 0);
+      steps[ps + __popcll(mu & below)] = make_int2(pt->tile_tok0[n], info);
+    }
+    p0 += __popcll(ma);
+    p1 += __popcll(mb);
+    ps += __popcll(mu);
+  }
+};
+
+__global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt,
+                                                    const uint8_t* __restrict__ la,
                                                     const uint8_t* __restrict__ ca,
                                                     const int32_t* __restrict__ row_ptr,
                                                     int32_t* __restrict__ col) {
-  const int64_t M = pt.num_tiles;
   const int lane = threadIdx.x & 63;
-  const int64_t r = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
-  if (r >= M * pt.num_q_heads) return;  // uniform per wavefront
-  const int h = static_cast<int>(r / M);
-  const int m = static_cast<int>(r - static_cast<int64_t>(h) * M);
-  const int s = pt.tile_seg[m];
-  int32_t pos = row_ptr[r];
+  const int u = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (u >= wt.num_units) return;  // uniform per wavefront
+  const int h = wt.unit_head[u];
+  const int m0 = wt.unit_m0[u];
+  const int m1 = wt.unit_m1[u];
+  const bool two = m1 >= 0;
+  const int64_t r0 = static_cast<int64_t>(h) * pt.num_tiles + m0;
+  Emitter e;
+  e.col = col;
+  e.steps = wt.steps;
+  e.pt = &pt;
+  e.p0 = row_ptr[r0];
+  e.p1 = two ? row_ptr[r0 + 1] : 0;
+  e.ps = wt.step_off[u];
+  e.m0 = m0;
+  e.m1 = m1;
+  e.lane = lane;
+  e.below = (1ull << lane) - 1ull;
+  const int s = pt.tile_seg[m0];
   if (pt.seg_kind[s] == kQuery) {
-    const int n0 = pt.tile_lo[m];
-    const int cnt = m - n0 + 1;
-    for (int k = lane; k < cnt; k += 64) col[pos + k] = n0 + k;
-    return;
+    // every tile of the prompt up to the M-block (Section 5.1)
+    const int lo = pt.tile_lo[m0];
+    for (int k0 = lo; k0 <= m0; k0 += 64) {
+      const int n = k0 + lane;
+      const bool ok = n <= m0;
+      e.emit(ok, ok && two, n);
+    }
+  } else {
+    // CA pages of every earlier document: shared by both M-blocks
+    for (int d = pt.seg_first[s]; d < s; ++d) {
+      const int Pe = pt.seg_pages[d];
+      const uint8_t* cav = ca + pt.seg_ca_off[d] + static_cast<int64_t>(h) * ca_nbytes(Pe);
+      for (int c0 = 0; c0 < Pe; c0 += 64) {
+        const int b = c0 + lane;
+        const bool on = b < Pe && get_bit(cav, b);
+        e.emit(on, on && two, pt.seg_tile0[d] + b);
+      }
+    }
+    // LA row i (m0) and row i+1 (m1), tiles j = 0..i; j == i is m0's diagonal
+    const int i = m0 - pt.seg_tile0[s];
+    const int P = pt.seg_pages[s];
+    const uint8_t* lav = la + pt.seg_la_off[s] + static_cast<int64_t>(h) * la_nbytes(P);
+    const int row_a = i * (i + 1) / 2;
+    const int row_b = (i + 1) * (i + 2) / 2;
+    for (int c0 = 0; c0 <= i; c0 += 64) {
+      const int j = c0 + lane;
+      const bool in = j <= i;
+      const bool a = in && (j == i || get_bit(lav, row_a + j));
+      const bool b = in && two && get_bit(lav, row_b + j);
+      e.emit(a, b, pt.seg_tile0[s] + j);
+    }
   }
-  for (int e = pt.seg_first[s]; e < s; ++e) {
-    const int Pe = pt.seg_pages[e];
-    const uint8_t* cav = ca + pt.seg_ca_off[e] + static_cast<int64_t>(h) * ca_nbytes(Pe);
-    pos = emit_bits(cav, 0, Pe, pt.seg_tile0[e], pos, lane, col);
+  if (two) e.emit(false, lane == 0, m1);  // m1's diagonal
+  if (lane == 0) wt.step_cnt[u] = e.ps - wt.step_off[u];
+}
+
+// Generic merge of caller-given lists (one thread per unit): the union of
+// rows m0 and m1, ascending, entries outside [first tile of the prompt,
+// M-block] skipped, at most step_off[u+1] - step_off[u] steps.
+__global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
+                                                   const int32_t* __restrict__ row_ptr,
+                                                   const int32_t* __restrict__ col,
+                                                   int64_t cap) {
+  const int u = blockIdx.x * blockDim.x + threadIdx.x;
+  if (u >= wt.num_units) return;
+  const int h = wt.unit_head[u];
+  const int m0 = wt.unit_m0[u];
+  const int m1 = wt.unit_m1[u];
+  const int lo = pt.tile_lo[m0];
+  const int64_t r0 = static_cast<int64_t>(h) * pt.num_tiles + m0;
+  auto clampi = [cap](int64_t x) { return min(cap, max(static_cast<int64_t>(0), x)); };
+  int64_t ia = clampi(row_ptr[r0]);
+  const int64_t ea = max(ia, clampi(row_ptr[r0 + 1]));
+  int64_t ib = 0, eb = 0;
+  if (m1 >= 0) {
+    ib = clampi(row_ptr[r0 + 1]);
+    eb = max(ib, clampi(row_ptr[r0 + 2]));
   }
-  const int i = m - pt.seg_tile0[s];
-  const int P = pt.seg_pages[s];
-  const uint8_t* lav = la + pt.seg_la_off[s] + static_cast<int64_t>(h) * la_nbytes(P);
-  pos = emit_bits(lav, i * (i + 1) / 2, i, pt.seg_tile0[s], pos, lane, col);
-  if (lane == 0) col[pos] = m;
+  const int base = wt.step_off[u];
+  const int room = wt.step_off[u + 1] - base;
+  int ns = 0;
+  while (ns < room) {
+    int na = 0x7fffffff, nb = 0x7fffffff;
+    while (ia < ea) {
+      const int n = col[ia];
+      if (n >= lo && n <= m0) { na = n; break; }
+      ++ia;
+    }
+    while (ib < eb) {
+      const int n = col[ib];
+      if (n >= lo && n <= m1) { nb = n; break; }
+      ++ib;
+    }
+    const int n = min(na, nb);
+    if (n == 0x7fffffff) break;
+    const bool a = na == n, b = nb == n;
+    if (a) ++ia;
+    if (b) ++ib;
+    const int info = pt.tile_len[n] | (a ? kStepIn0 : 0) | (b ? kStepIn1 : 0) |
+                     (n == m0 ? kStepDiag0 : 0) | (n == m1 ? kStepDiag1 : 0);
+    wt.steps[base + ns] = make_int2(pt.tile_tok0[n], info);
+    ++ns;
+  }
+  wt.step_cnt[u] = ns;
 }
 
 }  // namespace
 
-hipError_t launch_decode(const PlanTables& pt, const uint8_t* la, const uint8_t* ca,
-                         int32_t* counts, int32_t* row_ptr, int32_t* col_idx,
+hipError_t launch_decode(const PlanTables& pt, const WorkTables& wt, const uint8_t* la,
+                         const uint8_t* ca, int32_t* counts, int32_t* row_ptr, int32_t* col_idx,
                          hipStream_t stream) {
   const int64_t rows = static_cast<int64_t>(pt.num_tiles) * pt.num_q_heads;
   if (rows == 0) {  // empty layout: the scan alone writes row_ptr[0] = 0
@@ -169,8 +270,17 @@ hipError_t launch_decode(const PlanTables& pt, const uint8_t* la, const uint8_t*
   hipLaunchKernelGGL(decode_scan, dim3(1), dim3(1024), 0, stream, counts, row_ptr, rows);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(decode_write, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0,
-                     stream, pt, la, ca, row_ptr, col_idx);
+  if (wt.num_units == 0) return hipSuccess;
+  hipLaunchKernelGGL(decode_write, dim3(static_cast<unsigned>((wt.num_units + 3) / 4)), dim3(256),
+                     0, stream, pt, wt, la, ca, row_ptr, col_idx);
+  return hipGetLastError();
+}
+
+hipError_t launch_merge_steps(const PlanTables& pt, const WorkTables& wt, const int32_t* row_ptr,
+                              const int32_t* col_idx, int64_t col_capacity, hipStream_t stream) {
+  if (wt.num_units == 0) return hipSuccess;
+  hipLaunchKernelGGL(merge_steps, dim3(static_cast<unsigned>((wt.num_units + 255) / 256)),
+                     dim3(256), 0, stream, pt, wt, row_ptr, col_idx, col_capacity);
   return hipGetLastError();
 }
 

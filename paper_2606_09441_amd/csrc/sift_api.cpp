@@ -40,6 +40,11 @@ struct sift_plan {
 };
 
 namespace {
+// Everything an attention launch needs from the plan.
+sift::WorkTables work(const sift_plan* p) { return p->wt; }
+}  // namespace
+
+namespace {
 
 sift_status check_tensor(const sift_tensor* t, int32_t tokens, int32_t heads, int32_t dim) {
   if (t == nullptr) return SIFT_E_NULL;
@@ -75,7 +80,7 @@ sift_status check_io(const sift_tensor* q, const sift_tensor* k, const sift_tens
 struct HostPlan {
   std::vector<int32_t> seg_tile0, seg_pages, seg_kind, seg_first, seg_la_off, seg_ca_off;
   std::vector<int32_t> tile_seg, tile_tok0, tile_len, tile_lo;
-  std::vector<int32_t> unit_head, unit_m0, unit_m1, sched;
+  std::vector<int32_t> unit_head, unit_m0, unit_m1, sched, step_off;
   int64_t dense_tiles = 0;  // causal tiles of all prompts, one head
   int64_t la_bytes = 0, ca_bytes = 0;
   int32_t num_tokens = 0, num_segments = 0, num_tiles = 0;
@@ -193,6 +198,13 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
         order.push_back(u);
         ++u;
       }
+  // Each unit's merged step list has room for both M-blocks' causal tiles.
+  hp.step_off.assign(U + 1, 0);
+  for (int64_t k = 0; k < U; ++k) {
+    const int32_t m0 = hp.unit_m0[k], m1 = hp.unit_m1[k];
+    const int32_t lo = hp.tile_lo[m0];
+    hp.step_off[k + 1] = hp.step_off[k] + (m0 - lo + 1) + (m1 >= 0 ? m1 - lo + 1 : 0);
+  }
   // Split the locality order into kNumXcd contiguous chunks; workgroup
   // x + kNumXcd * k runs chunk x's k-th unit (longest first inside a chunk).
   std::vector<std::vector<int32_t>> chunk(kNumXcd);
@@ -263,12 +275,18 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   const size_t o_uh = put(blob, hp.unit_head);
   const size_t o_um0 = put(blob, hp.unit_m0);
   const size_t o_um1 = put(blob, hp.unit_m1);
+  const size_t o_soff = put(blob, hp.step_off);
   const int64_t rows = static_cast<int64_t>(hp.num_tiles) * num_q_heads;
   const int64_t cap = hp.dense_tiles * num_q_heads;
-  const size_t o_counts = (blob.size() + 255) & ~size_t(255);
-  const size_t o_rowptr = (o_counts + rows * 4 + 255) & ~size_t(255);
-  const size_t o_col = (o_rowptr + (rows + 1) * 4 + 255) & ~size_t(255);
-  const size_t total = o_col + std::max<int64_t>(cap, 1) * 4;
+  const int64_t U = static_cast<int64_t>(hp.unit_head.size());
+  auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
+  const size_t o_counts = align(blob.size());
+  const size_t o_rowptr = align(o_counts + rows * 4);
+  const size_t o_col = align(o_rowptr + (rows + 1) * 4);
+  const size_t o_scnt = align(o_col + std::max<int64_t>(cap, 1) * 4);
+  const size_t o_steps = align(o_scnt + std::max<int64_t>(U, 1) * 4);
+  // steps: the units' lists, plus a few entries read (never used) past the end
+  const size_t total = o_steps + (std::max<int64_t>(cap, 1) + 8) * 8;
 
   sift_plan* plan = new (std::nothrow) sift_plan();
   if (plan == nullptr) return SIFT_E_HIP;
@@ -306,6 +324,10 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   plan->wt.unit_head = P(o_uh);
   plan->wt.unit_m0 = P(o_um0);
   plan->wt.unit_m1 = P(o_um1);
+  plan->wt.step_off = P(o_soff);
+  plan->wt.step_cnt = P(o_scnt);
+  plan->wt.steps = reinterpret_cast<int2*>(P(o_steps));
+  plan->wt.num_units = static_cast<int32_t>(U);
   plan->wt.grid = static_cast<int32_t>(hp.sched.size());
   plan->counts = P(o_counts);
   plan->row_ptr = P(o_rowptr);
@@ -356,9 +378,17 @@ sift_status sift_decode_tiles(sift_plan* plan, const uint8_t* local_bitmap,
   if (col_capacity < plan->info.list_capacity) return SIFT_E_CAPACITY;
   sift_status st = check_device(plan);
   if (st != SIFT_OK) return st;
-  const hipError_t e = sift::launch_decode(plan->pt, local_bitmap, cross_bitmap, plan->counts,
-                                           row_ptr, col_idx, static_cast<hipStream_t>(stream));
+  const hipError_t e = sift::launch_decode(plan->pt, work(plan), local_bitmap, cross_bitmap,
+                                           plan->counts, row_ptr, col_idx,
+                                           static_cast<hipStream_t>(stream));
   return e == hipSuccess ? SIFT_OK : SIFT_E_HIP;
+}
+
+sift_status sift_plan_decode(sift_plan* plan, const uint8_t* local_bitmap,
+                             const uint8_t* cross_bitmap, void* stream) {
+  if (plan == nullptr) return SIFT_E_NULL;
+  return sift_decode_tiles(plan, local_bitmap, cross_bitmap, plan->row_ptr, plan->col_idx,
+                           plan->info.list_capacity, stream);
 }
 
 sift_status sift_sparse_attention(sift_plan* plan, const sift_tensor* q, const sift_tensor* k,
@@ -391,8 +421,45 @@ sift_status sift_sparse_attention(sift_plan* plan, const sift_tensor* q, const s
   a.scale_log2 = softmax_scale * 1.4426950408889634f;
   a.out_f32 = out->dtype == SIFT_F32 ? 1 : 0;
   const hipStream_t s = static_cast<hipStream_t>(stream);
-  const hipError_t e = bf16 ? sift::launch_attn_bf16(plan->pt, plan->wt, a, s)
-                            : sift::launch_attn_f32(plan->pt, a, s);
+  hipError_t e;
+  if (bf16) {
+    // the bf16 kernel walks merged per-unit step lists: build them from the lists
+    e = sift::launch_merge_steps(plan->pt, work(plan), row_ptr, col_idx, col_capacity, s);
+    if (e == hipSuccess) e = sift::launch_attn_bf16(plan->pt, work(plan), a, s);
+  } else {
+    e = sift::launch_attn_f32(plan->pt, a, s);
+  }
+  return e == hipSuccess ? SIFT_OK : SIFT_E_HIP;
+}
+
+sift_status sift_plan_attention(sift_plan* plan, const sift_tensor* q, const sift_tensor* k,
+                                const sift_tensor* v, float softmax_scale, sift_tensor* out,
+                                void* stream) {
+  if (plan == nullptr) return SIFT_E_NULL;
+  const sift_plan_info& in = plan->info;
+  sift_status st = check_io(q, k, v, out, in.num_tokens, in.num_q_heads, in.num_kv_heads,
+                            in.head_dim, in.tile);
+  if (st != SIFT_OK) return st;
+  if ((st = check_device(plan)) != SIFT_OK) return st;
+  if (!(softmax_scale > 0.f) || !std::isfinite(softmax_scale))
+    softmax_scale = 1.0f / std::sqrt(static_cast<float>(in.head_dim));
+  sift::AttnArgs a{};
+  a.q = q->data;
+  a.k = k->data;
+  a.v = v->data;
+  a.out = out->data;
+  a.row_ptr = plan->row_ptr;
+  a.col_idx = plan->col_idx;
+  a.col_capacity = in.list_capacity;
+  a.hq = in.num_q_heads;
+  a.hkv = in.num_kv_heads;
+  a.head_dim = in.head_dim;
+  a.tile = in.tile;
+  a.scale_log2 = softmax_scale * 1.4426950408889634f;
+  a.out_f32 = out->dtype == SIFT_F32 ? 1 : 0;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const hipError_t e = q->dtype == SIFT_BF16 ? sift::launch_attn_bf16(plan->pt, work(plan), a, s)
+                                             : sift::launch_attn_f32(plan->pt, a, s);
   return e == hipSuccess ? SIFT_OK : SIFT_E_HIP;
 }
 
@@ -408,11 +475,9 @@ sift_status sift_plan_run(sift_plan* plan, const sift_tensor* q, const sift_tens
   if (st != SIFT_OK) return st;
   if (in.la_bytes > 0 && local_bitmap == nullptr) return SIFT_E_NULL;
   if (in.ca_bytes > 0 && cross_bitmap == nullptr) return SIFT_E_NULL;
-  st = sift_decode_tiles(plan, local_bitmap, cross_bitmap, plan->row_ptr, plan->col_idx,
-                         in.list_capacity, stream);
+  st = sift_plan_decode(plan, local_bitmap, cross_bitmap, stream);
   if (st != SIFT_OK) return st;
-  return sift_sparse_attention(plan, q, k, v, plan->row_ptr, plan->col_idx, in.list_capacity,
-                               softmax_scale, out, stream);
+  return sift_plan_attention(plan, q, k, v, softmax_scale, out, stream);
 }
 
 sift_status sift_sparse_prefill(const sift_tensor* q, const sift_tensor* k, const sift_tensor* v,

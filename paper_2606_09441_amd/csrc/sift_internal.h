@@ -29,18 +29,39 @@ struct PlanTables {
 
 // Attention work: one unit = (query head, a pair of consecutive M-blocks of
 // one segment).  sched[g] is the unit run by workgroup g, or -1 for none.
+// A unit's merged step list (the union of its two M-blocks' lists, in
+// ascending key-tile order) lives at steps[step_off[u] ..
+// step_off[u] + step_cnt[u]); step_off[u+1] - step_off[u] bounds its length.
+// Step = {first token of the key tile, len | in0 << 8 | in1 << 9 |
+// (n == m0) << 10 | (n == m1) << 11}.
 struct WorkTables {
   const int32_t* sched;       // [grid]
   const int32_t* unit_head;   // [U]
   const int32_t* unit_m0;     // [U] first M-block
   const int32_t* unit_m1;     // [U] second M-block, or -1
+  const int32_t* step_off;    // [U + 1]
+  int32_t* step_cnt;          // [U] (device scratch)
+  int2* steps;                // [step_off[U]] (device scratch)
+  int32_t num_units;          // U
   int32_t grid;
 };
 
-// Decode (Section 5.1): count, scan, write.
-hipError_t launch_decode(const PlanTables& pt, const uint8_t* la, const uint8_t* ca,
-                         int32_t* counts, int32_t* row_ptr, int32_t* col_idx,
+constexpr int kStepLenMask = 0xff;
+constexpr int kStepIn0 = 1 << 8;
+constexpr int kStepIn1 = 1 << 9;
+constexpr int kStepDiag0 = 1 << 10;
+constexpr int kStepDiag1 = 1 << 11;
+
+// Decode (Section 5.1): count, scan, write.  The write pass runs per unit and
+// emits both M-blocks' lists and the unit's merged step list.
+hipError_t launch_decode(const PlanTables& pt, const WorkTables& wt, const uint8_t* la,
+                         const uint8_t* ca, int32_t* counts, int32_t* row_ptr, int32_t* col_idx,
                          hipStream_t stream);
+
+// Merged step lists from caller-given per-M-block lists (entries outside
+// [first tile of the prompt, M-block] skipped; lists ascending).
+hipError_t launch_merge_steps(const PlanTables& pt, const WorkTables& wt, const int32_t* row_ptr,
+                              const int32_t* col_idx, int64_t col_capacity, hipStream_t stream);
 
 struct AttnArgs {
   const void* q;
@@ -55,6 +76,7 @@ struct AttnArgs {
   int32_t out_f32;            // 1: fp32 output, 0: bf16 output
 };
 
+// bf16 attention reads the merged step lists of wt (not row_ptr/col_idx).
 hipError_t launch_attn_bf16(const PlanTables& pt, const WorkTables& wt, const AttnArgs& a,
                             hipStream_t stream);
 hipError_t launch_attn_f32(const PlanTables& pt, const AttnArgs& a, hipStream_t stream);

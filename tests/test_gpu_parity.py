@@ -240,3 +240,49 @@ def test_decode_capacity_is_checked():
         assert e.value.status == 5
     finally:
         dw.close()
+
+
+def test_attention_over_given_lists_matches_plan_run():
+    """sift_sparse_attention (lists given by the caller, merged on the
+    device) and sift_plan_run (lists decoded from the bits) agree exactly,
+    also when the given lists are padded with out-of-range entries."""
+    wl = W.custom([[300, 64, 129, 75], [5], [1, 64, 0], [200, 131, 70]], tile=64, hq=8, hkv=2,
+                  d=128, dtype="bf16", seed=7, p_la=0.4, p_ca=0.3)
+    dw = DevWorkload(wl)
+    try:
+        a = dw.run()
+        rp, ci = dw.plan.decode(dw.la, dw.ca)
+        b = dw.plan.attention(dw.q, dw.k, dw.v, rp, ci)
+        torch.cuda.synchronize()
+        assert torch.equal(a, b)
+        # the same lists with entries that must be skipped: a tile of another
+        # prompt and a tile after the M-block, inserted in every list
+        rph = rp.cpu().numpy().astype(np.int64)
+        cih = ci.cpu().numpy()[: rph[-1]]
+        M = dw.plan.info["num_tiles"]
+        new_rp, new_ci = [0], []
+        for r in range(len(rph) - 1):
+            m = r % M
+            lst = cih[rph[r]:rph[r + 1]].tolist()
+            new_ci.extend([-5] + lst + [M + 3])
+            new_rp.append(len(new_ci))
+        rp2 = torch.tensor(new_rp, dtype=torch.int32, device=dw.q.device)
+        ci2 = torch.tensor(new_ci, dtype=torch.int32, device=dw.q.device)
+        c = dw.plan.attention(dw.q, dw.k, dw.v, rp2, ci2)
+        torch.cuda.synchronize()
+        assert torch.equal(a, c)
+    finally:
+        dw.close()
+
+
+def test_plan_decode_then_attention_matches_run():
+    wl = workload("llama8b_4k")
+    dw = DevWorkload(wl)
+    try:
+        a = dw.run()
+        dw.plan.decode_internal(dw.la, dw.ca)
+        b = dw.plan.attention_internal(dw.q, dw.k, dw.v)
+        torch.cuda.synchronize()
+    finally:
+        dw.close()
+    assert torch.equal(a, b)
