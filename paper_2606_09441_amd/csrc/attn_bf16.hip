@@ -25,15 +25,23 @@
 //    4q..4q+3).
 //  * K and V tiles are staged in LDS as unpadded 256 B rows with an XOR
 //    swizzle of the 16-byte chunks (K: chunk ^ (row & 15), V: chunk ^
-//    4(row & 3)) so that the MFMA operand reads are free of bank conflicts;
-//    16 consecutive lanes store one row.  Global loads are buffer loads
-//    through a per-tile resource that ends at the tile's last valid row:
-//    rows past the end of a partial tile arrive as zeros.
-//  * Double-buffered staging, one barrier per tile: the loads of step t+1's
-//    K and V are issued into registers at the start of step t, step t is
-//    computed from LDS, and the registers are stored into the other buffer
-//    at its end.  Two workgroups per CU (2 wavefronts per SIMD) let one
-//    wavefront's MFMAs overlap the other's softmax.
+//    4(row & 3)) so that the MFMA operand reads are free of bank conflicts.
+//    They are copied by the LDS DMA form of the buffer load (each lane's 16
+//    bytes land at M0 + 16 * lane, so the swizzle is applied to the global
+//    address), through a per-tile resource that ends at the tile's last
+//    valid row: rows past the end of a partial tile arrive as zeros.  No
+//    registers hold staged data.  The DMA is issued as inline assembly and
+//    waited for explicitly before the step's barrier: the compiler, which
+//    cannot tell the DMA target from the buffers being read, would otherwise
+//    wait for it before every LDS read.
+//  * Software pipeline, one barrier per step.  During step t a wavefront
+//    computes S(t+1) = K(t+1) Q^T on the MFMA pipe while the VALU turns S(t)
+//    into P(t) (exp2, bf16 rounding, row sum), then O += V(t)^T P(t) on the
+//    MFMA pipe while the VALU reduces the row max of S(t+1).  Meanwhile the
+//    DMA brings K(t+2) and V(t+1): K runs one tile ahead of V, each with two
+//    LDS slots (a slot is refilled only after the barrier that follows its
+//    last read).  Two workgroups per CU (2 wavefronts per SIMD) cover the
+//    remaining stalls.
 //  * Online softmax in the log2 domain with a lazy reference max (rescale
 //    only when a tile's max exceeds it by more than kLazy); P is rounded to
 //    bf16 and the row sum adds exactly those rounded values
@@ -43,6 +51,8 @@
 //    grouped per XCD (workgroups go round-robin over the 8 XCDs) so that the
 //    query heads sharing a kv head, and the M-blocks sharing key pages, run
 //    on one L2; longest lists first.
+
+#include <type_traits>
 
 #include "sift_internal.h"
 
@@ -56,6 +66,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 typedef __attribute__((address_space(3))) __bf16 lds_bf16;
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
@@ -101,40 +112,53 @@ __device__ __forceinline__ Step make_step(int2 x, bool valid) {
   return s;
 }
 
-// Global -> registers: thread t loads, for it = 0..3, row 16*(t/64) + 4it +
-// (t%64)/16 of the tile, logical 16-byte chunk (t%16) ^ swizzle(row), which
-// it later stores at physical chunk t%16 of that row (koff/voff are the
-// per-thread byte offsets of those chunks).
-__device__ __forceinline__ void load_tile(u32x4 (&r)[4], const __bf16* __restrict__ base, int len,
-                                          int row_bytes, const int (&off)[4]) {
-  const int valid = (len - 1) * row_bytes + kD * 2;  // through the last valid row
-  const __amdgpu_buffer_rsrc_t rs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<__bf16*>(base), 0, valid, kBufferWord3);
-#pragma unroll
-  for (int it = 0; it < 4; ++it)
-    r[it] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, off[it], 0, 0));
+// Buffer resource of one key tile of one kv head: base = its first row,
+// num_records = bytes through the last valid row (loads past it return 0).
+__device__ __forceinline__ i32x4 tile_rsrc(const __bf16* base, int len, int row_bytes) {
+  const unsigned long long a = reinterpret_cast<unsigned long long>(base);
+  const int valid = (len - 1) * row_bytes + kD * 2;
+  return i32x4{static_cast<int>(static_cast<unsigned>(a)), static_cast<int>((a >> 32) & 0xffff),
+               valid, kBufferWord3};
 }
 
-// Registers -> LDS: 16 consecutive lanes write one 256 B row.
-__device__ __forceinline__ void store_tile(const u32x4 (&r)[4], lds_bf16* dst) {
-#pragma unroll
-  for (int it = 0; it < 4; ++it)
-    *reinterpret_cast<__attribute__((address_space(3))) u32x4*>(dst + it * 4 * kD) = r[it];
+// Global -> LDS, 16 bytes per lane from byte voff of the resource, landing
+// at m0 + 16 * lane.
+__device__ __forceinline__ void dma_b128(int m0, int voff, const i32x4& rs) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(m0), "v"(voff), "s"(rs)
+               : "memory", "m0");
 }
+
+// One wavefront's quarter of a tile: rows 16w + 4it + lane/16 (it = 0..3),
+// physical chunk lane % 16 of each.  off0 is the lane's global byte offset
+// for it = 0; rows 4it further down sit it * rstep bytes further, and their
+// logical chunk differs by an XOR of the chunk index with xsw(it) (bits 6-7
+// of the byte offset; the row part is a multiple of 256).  row0 = LDS byte
+// address of row 16w.
+template <bool kXor>
+__device__ __forceinline__ void dma_tile(int row0, int off0, int rstep, const i32x4& rs) {
+#pragma unroll
+  for (int it = 0; it < 4; ++it) {
+    const int off = (kXor ? (off0 ^ (it << 6)) : off0) + it * rstep;
+    dma_b128(row0 + it * 4 * kD * 2, off, rs);
+  }
+}
+
+__device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // A operand of S^T = K Q^T: lane (l32, hf) reads row 32kb + l32, logical
-// 16-byte chunk 2s + hf, stored at chunk (2s + hf) ^ (row & 15).
+// 16-byte chunk 2s + hf, stored at chunk (2s + hf) ^ (row & 15).  With x =
+// (l32 & 15) >> 1 the byte offset inside the row is 32(s ^ x) + 16(hf ^
+// (l32 & 1)): the lane's address for s = 0 XORed with 32s (bits 5-7 of an
+// address whose row part is a multiple of 256).
 struct QkArgs {
-  const lds_bf16* ks;
-  int row0;  // l32 * kD
-  int sw;    // l32 & 15 (== row & 15 for both 32-row blocks)
-  int hf;
+  int addr;  // LDS byte address of k-step 0, block 0, in K slot 0
 };
 
-__device__ __forceinline__ bf16x8 k_frag(const QkArgs& q, int kb, int s) {
-  const int chunk = (2 * s + q.hf) ^ q.sw;
-  const lds_bf16* p = q.ks + q.row0 + kb * 32 * kD + chunk * 8;
-  return as_bf16x8(*reinterpret_cast<const lds_u32x4*>(p));
+__device__ __forceinline__ bf16x8 k_frag(const QkArgs& q, int slot_off, int kb, int s) {
+  const int a = (q.addr ^ (s << 5)) + slot_off + kb * 32 * kD * 2;
+  return as_bf16x8(*reinterpret_cast<const lds_u32x4*>(static_cast<size_t>(a)));
 }
 
 // V^T operand of O^T += V^T P^T for head-dim block db and key step st: lane
@@ -142,33 +166,32 @@ __device__ __forceinline__ bf16x8 k_frag(const QkArgs& q, int kb, int s) {
 // 16st + 8 + 4hf + {0..3}: two transpose reads of 4-row blocks.  Lane l is
 // the source lane of row (l & 15) >> 2 of each block, columns 32db +
 // 16((l >> 4) & 1) + 4(l & 3) .. +3; the V swizzle XORs the 16-byte chunk
-// with 4 * (row & 3) = 4 * ((l & 15) >> 2), constant per lane.
+// with 4 * (row & 3) = 4 * ((l & 15) >> 2), constant per lane.  In bytes the
+// column part is 64(db ^ ((l & 15) >> 2)) + 32((l >> 4) & 1) + 8(l & 3), so
+// the address for db is the lane's address for db = 0 XORed with 64db.
 struct PvArgs {
-  const lds_bf16* vs;
-  int row0;   // (((l & 15) >> 2) + 4hf) * kD
-  int cbase;  // 16((l >> 4) & 1) + 4(l & 3)
-  int sw;     // 4 * ((l & 15) >> 2)
+  int addr;  // LDS byte address of db = 0, st = 0, first block, in V slot 0
 };
 
-__device__ __forceinline__ bf16x8 v_frag(const PvArgs& v, int db, int st) {
-  const int col = 32 * db + v.cbase;                    // logical column of the 8 B piece
-  const int pc = ((col >> 3) ^ v.sw) * 8 + (col & 7);   // swizzled element column
-  const lds_bf16* p0 = v.vs + v.row0 + 16 * st * kD + pc;
-  const lds_bf16* p1 = p0 + 8 * kD;  // keys + 8: row & 3 unchanged, same swizzle
-  const bf16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p0);
-  const bf16x4 y = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p1);
+__device__ __forceinline__ bf16x8 v_frag(const PvArgs& v, int slot_off, int db, int st) {
+  const int a = (v.addr ^ (db << 6)) + slot_off + 16 * st * kD * 2;
+  const bf16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      reinterpret_cast<lds_bf16x4*>(static_cast<size_t>(a)));
+  // keys + 8: row & 3 unchanged, same swizzle
+  const bf16x4 y = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      reinterpret_cast<lds_bf16x4*>(static_cast<size_t>(a + 8 * kD * 2)));
   return bf16x8{x[0], x[1], x[2], x[3], y[0], y[1], y[2], y[3]};
 }
 
-__device__ __forceinline__ void qk_tile(const QkArgs& q, const bf16x8 (&qf)[8], f32x16& s0,
-                                        f32x16& s1) {
-  bf16x8 a0 = k_frag(q, 0, 0), a1 = k_frag(q, 1, 0);
+__device__ __forceinline__ void qk_tile(const QkArgs& q, int slot_off, const bf16x8 (&qf)[8],
+                                        f32x16& s0, f32x16& s1) {
+  bf16x8 a0 = k_frag(q, slot_off, 0, 0), a1 = k_frag(q, slot_off, 1, 0);
   s0 = mfma(a0, qf[0], f32x16{});
   s1 = mfma(a1, qf[0], f32x16{});
 #pragma unroll
   for (int s = 1; s < 8; ++s) {
-    a0 = k_frag(q, 0, s);
-    a1 = k_frag(q, 1, s);
+    a0 = k_frag(q, slot_off, 0, s);
+    a1 = k_frag(q, slot_off, 1, s);
     s0 = mfma(a0, qf[s], s0);
     s1 = mfma(a1, qf[s], s1);
   }
@@ -204,28 +227,40 @@ struct RowState {
   float lsum;   // this lane's share of the row sum
 };
 
-// Mask (diagonal / partial tile) and lazy-rescale step of the softmax for
-// scores s0/s1 of a tile this wavefront computes.  Returns the exp base.
-__device__ __forceinline__ float softmax_prepare(f32x16& s0, f32x16& s1, RowState& st,
-                                                 const Step& cur, int wave, int qrow, int hf,
-                                                 float c) {
-  const bool diag = cur.diag(wave);
-  if (diag || cur.len() < kT) {
-    // key of value v of block kb: 32kb + 8(v>>2) + 4hf + (v&3)
-    const int klim = cur.len() - 4 * hf;
-    const int qlim = diag ? qrow - 4 * hf : 1 << 20;
+// Scores of keys past the end of a partial tile, or after the query on the
+// diagonal tile, become -inf.  Value v of block kb holds key 32kb + 8(v>>2)
+// + 4hf + (v&3).
+__device__ __forceinline__ void mask_tile(f32x16& s0, f32x16& s1, const Step& st, int wave,
+                                          int qrow, int hf, bool all = false) {
+  const int klim = all ? -64 : st.len() - 4 * hf;
+  const int qlim = st.diag(wave) ? qrow - 4 * hf : 1 << 20;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int kc = 8 * (v >> 2) + (v & 3);
-      if (kc >= klim || kc > qlim) s0[v] = -INFINITY;
-      if (kc + 32 >= klim || kc + 32 > qlim) s1[v] = -INFINITY;
-    }
+  for (int v = 0; v < 16; ++v) {
+    const int kc = 8 * (v >> 2) + (v & 3);
+    if (kc >= klim || kc > qlim) s0[v] = -INFINITY;
+    if (kc + 32 >= klim || kc + 32 > qlim) s1[v] = -INFINITY;
   }
-  float mx = fmaxf(s0[0], s1[0]);
+}
+
+__device__ __forceinline__ bool needs_mask(const Step& st, int wave) {
+  return st.diag(wave) || st.len() < kT;
+}
+
+// Row max of a score tile (both lane halves of the row agree).
+__device__ __forceinline__ float tile_max(const f32x16& s0, const f32x16& s1) {
+  float m0 = fmaxf(s0[0], s1[0]);
+  float m1 = fmaxf(s0[1], s1[1]);
 #pragma unroll
-  for (int v = 1; v < 16; ++v) mx = fmaxf(mx, fmaxf(s0[v], s1[v]));
-  mx = swap_max(mx);
-  const float mxs = mx * c;
+  for (int v = 2; v < 16; v += 2) {
+    m0 = __builtin_fmaxf(m0, __builtin_fmaxf(s0[v], s1[v]));
+    m1 = __builtin_fmaxf(m1, __builtin_fmaxf(s0[v + 1], s1[v + 1]));
+  }
+  return swap_max(fmaxf(m0, m1));
+}
+
+// Lazy rescale: move the reference max (and rescale O and l) only when the
+// tile's scaled max mxs exceeds it by more than kLazy.
+__device__ __forceinline__ void rescale(RowState& st, float mxs) {
   const bool grow = mxs > st.mref + kLazy;
   if (__builtin_amdgcn_ballot_w64(grow)) {
     const float mnew = grow ? mxs : st.mref;
@@ -237,6 +272,9 @@ __device__ __forceinline__ float softmax_prepare(f32x16& s0, f32x16& s1, RowStat
 #pragma unroll
       for (int v = 0; v < 16; ++v) st.o[db][v] *= alpha;
   }
+}
+
+__device__ __forceinline__ float exp_base(const RowState& st) {
   return st.mref == -INFINITY ? 0.f : st.mref;
 }
 
@@ -264,11 +302,47 @@ __device__ __forceinline__ void softmax_exp(const f32x16& s0, const f32x16& s1, 
   lsum += psum;
 }
 
-__device__ __forceinline__ void pv_tile(const PvArgs& v, const bf16x8 (&pb)[4], RowState& st) {
+__device__ __forceinline__ void pv_tile(const PvArgs& v, int slot_off, const bf16x8 (&pb)[4],
+                                        RowState& st) {
 #pragma unroll
   for (int s = 0; s < 4; ++s)
 #pragma unroll
-    for (int db = 0; db < 4; ++db) st.o[db] = mfma(v_frag(v, db, s), pb[s], st.o[db]);
+    for (int db = 0; db < 4; ++db) st.o[db] = mfma(v_frag(v, slot_off, db, s), pb[s], st.o[db]);
+}
+
+// Interleave QK^T of the next tile (16 LDS reads, 16 MFMAs) with the
+// softmax exponentials of the current one, and PV of the current tile (32
+// transpose reads, 16 MFMAs) with the row max of the next one.
+__device__ __forceinline__ void interleave_qk_exp() {
+  __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if (i < 14) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x402, 6, 0);
+  }
+}
+
+__device__ __forceinline__ void interleave_pv_max() {
+  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if (i < 14) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x402, 2, 0);
+  }
+}
+
+// The same with nothing to interleave: keep the fragment reads two MFMAs
+// ahead (an unconstrained schedule issues all of them first and runs out of
+// registers).
+__device__ __forceinline__ void pace_qk() {
+  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if (i < 12) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
 }
 
 template <bool kOutF32>
@@ -299,23 +373,24 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
   const __bf16* __restrict__ kp = static_cast<const __bf16*>(a.k);
   const __bf16* __restrict__ vp = static_cast<const __bf16*>(a.v);
   lds_bf16* lds = (lds_bf16*)smem;
-  lds_bf16* const kslot[2] = {lds, lds + kTile};
-  lds_bf16* const vslot[2] = {lds + 2 * kTile, lds + 3 * kTile};
+  // LDS byte addresses of this wavefront's first DMA row in each slot
+  const int lds0 = static_cast<int>(reinterpret_cast<size_t>(lds)) + 16 * wave * kD * 2;
+  const int kdst[2] = {lds0, lds0 + 2 * kTile};
+  const int vdst[2] = {lds0 + 4 * kTile, lds0 + 6 * kTile};
 
-  // global byte offsets: row 16w + 4it + l/16, logical chunk (l%16) ^
-  // swizzle(row); this thread stores at element 16w*kD + it*4*kD + 8l.
-  int koff[4], voff[4];
+  // global byte offsets of the DMA rows 16w + 4it + l/16, logical chunk
+  // (l%16) ^ swizzle(row), which lands at physical chunk l%16 of that row.
+  // K: swizzle = row & 15 = 4it + l/16, so the chunk for it is the chunk for
+  // it = 0 XOR 4it.  V: swizzle = 4(row & 3) = 4(l/16), the same for every it.
+  int koff0, voff0;
   {
     const int rsub = lane >> 4;
     const int pc = lane & 15;
-#pragma unroll
-    for (int it = 0; it < 4; ++it) {
-      const int row = 16 * wave + 4 * it + rsub;
-      koff[it] = row * row_bytes + ((pc ^ (row & 15)) * 16);
-      voff[it] = row * row_bytes + ((pc ^ (4 * (row & 3))) * 16);
-    }
+    const int row = 16 * wave + rsub;
+    koff0 = row * row_bytes + ((pc ^ rsub) * 16);
+    voff0 = row * row_bytes + ((pc ^ (4 * rsub)) * 16);
   }
-  const int st_off = 16 * wave * kD + 8 * lane;
+  const int rstep = 4 * row_bytes;
 
   // Q^T fragments (B operand of S^T = K Q^T): lane holds query row qrow,
   // dims 16s + 8hf .. +7 for k-step s.
@@ -340,8 +415,9 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
   const int2* __restrict__ steps = wt.steps + wt.step_off[unit];
   const int nsteps = wt.step_cnt[unit];
   const int64_t kv_head_off = static_cast<int64_t>(kvh) * kD;
-  auto tile_ptr = [&](const __bf16* base, const Step& s) {
-    return base + static_cast<int64_t>(s.tok0) * kstride + kv_head_off;
+  auto rsrc = [&](const __bf16* base, const Step& s) {
+    return tile_rsrc(base + static_cast<int64_t>(s.tok0) * kstride + kv_head_off, s.len(),
+                     row_bytes);
   };
   auto fetch = [&](int i) { return steps[i < nsteps ? i : 0]; };
 
@@ -353,55 +429,105 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
   rs.mref = -INFINITY;
   rs.lsum = 0.f;
 
+  const int lds_base = static_cast<int>(reinterpret_cast<size_t>(lds));
   QkArgs qa;
-  qa.row0 = l32 * kD;
-  qa.sw = l32 & 15;
-  qa.hf = hf;
+  qa.addr = lds_base + l32 * kD * 2 + 32 * ((l32 & 15) >> 1) + 16 * (hf ^ (l32 & 1));
   PvArgs pva;
-  pva.row0 = (((lane & 15) >> 2) + 4 * hf) * kD;
-  pva.cbase = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-  pva.sw = 4 * ((lane & 15) >> 2);
-
-  // ---- prologue: stage step 0
-  // (an empty list leaves O = 0 and l = 0: the epilogue writes zeros)
-  u32x4 kr[4], vr[4];
-  Step cur = make_step(fetch(0), nsteps > 0);
-  int2 raw1 = fetch(1);
-  if (cur.valid) {
-    load_tile(kr, tile_ptr(kp, cur), cur.len(), row_bytes, koff);
-    load_tile(vr, tile_ptr(vp, cur), cur.len(), row_bytes, voff);
-    store_tile(kr, kslot[0] + st_off);
-    store_tile(vr, vslot[0] + st_off);
+  {
+    const int cbase = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+    const int z = (lane & 15) >> 2;
+    pva.addr = lds_base + 4 * kTile + (z + 4 * hf) * kD * 2 + 64 * z + 16 * (cbase >> 3) +
+               2 * (cbase & 7);
   }
-  __syncthreads();
 
-  int par = 0;
-  for (int t = 0; t < nsteps; ++t) {
-    // Step t+1's tiles go into registers now and into the other buffer
-    // after step t (past the end of the list: step t's tiles again, into a
-    // buffer nobody reads, so loads and stores stay unconditional).  The
-    // step after next is fetched here and decoded at the end of the step.
-    const Step nx = make_step(raw1, t + 1 < nsteps);
-    raw1 = fetch(t + 2);
-    const Step& ld = nx.valid ? nx : cur;
-    load_tile(kr, tile_ptr(kp, ld), ld.len(), row_bytes, koff);
-    load_tile(vr, tile_ptr(vp, ld), ld.len(), row_bytes, voff);
-
-    if (cur.in(wave)) {
-      qa.ks = kslot[par];
-      pva.vs = vslot[par];
-      f32x16 s0, s1;
-      qk_tile(qa, qf, s0, s1);
-      const float base = softmax_prepare(s0, s1, rs, cur, wave, qrow, hf, c);
-      bf16x8 pb[4];
-      softmax_exp(s0, s1, c, base, pb, rs.lsum);
-      pv_tile(pva, pb, rs);
-    }
-    store_tile(kr, kslot[par ^ 1] + st_off);
-    store_tile(vr, vslot[par ^ 1] + st_off);
+  // an empty list leaves O = 0 and l = 0: the epilogue writes zeros
+  if (nsteps > 0) {
+    // ---- prologue: K(0), V(0), K(1) into LDS; S(0) = K(0) Q^T
+    Step c0 = make_step(fetch(0), true);
+    Step c1 = make_step(fetch(1), nsteps > 1);
+    Step c2 = make_step(fetch(2), nsteps > 2);
+    dma_tile<true>(kdst[0], koff0, rstep, rsrc(kp, c0));
+    dma_tile<false>(vdst[0], voff0, rstep, rsrc(vp, c0));
+    dma_tile<true>(kdst[1], koff0, rstep, rsrc(kp, c1.valid ? c1 : c0));
+    wait_dma();
     __syncthreads();
-    cur = nx;
-    par ^= 1;
+    f32x16 sa0, sa1, sb0, sb1;  // score tiles of even / odd steps
+    if (c0.in(wave)) {
+      qk_tile(qa, 0, qf, sa0, sa1);
+      pace_qk();
+      if (needs_mask(c0, wave)) mask_tile(sa0, sa1, c0, wave, qrow, hf);
+      rescale(rs, tile_max(sa0, sa1) * c);
+    }
+    __syncthreads();  // K slot 0 is refilled by step 0
+
+    // ---- step t: S(t) is in (cur0, cur1); computes S(t+1) into (nx0, nx1)
+    auto step = [&](int t, const int par, f32x16& cur0, f32x16& cur1, f32x16& nx0,
+                    f32x16& nx1) {
+      // V(t+1) and K(t+2) (past the end of the list: step t's tiles again,
+      // into slots nobody reads, so the DMA stays unconditional)
+      dma_tile<false>(vdst[par ^ 1], voff0, rstep, rsrc(vp, c1.valid ? c1 : c0));
+      dma_tile<true>(kdst[par], koff0, rstep, rsrc(kp, c2.valid ? c2 : c0));
+      const int2 raw3 = fetch(t + 3);  // decoded after the DMA wait below
+      const bool a0 = c0.in(wave);
+      const bool a1 = c1.valid && c1.in(wave);
+      // keep the per-read addresses derived inside the step (hoisted out of
+      // the loop they would each hold a register)
+      asm volatile("" : "+v"(qa.addr), "+v"(pva.addr), "+v"(koff0), "+v"(voff0));
+      const int kso = (par ^ 1) * 2 * kTile;  // byte offset of K slot par ^ 1
+      const int vso = par * 2 * kTile;        // byte offset of V slot par
+      // one straight-line body per case.  When this wavefront's M-block lists
+      // tile t but not tile t+1 (or t is the last step), the full body runs
+      // and S(t+1) is masked out entirely: K(t+1) is only read, never
+      // weighted.  Without tile t, the body leaves out P(t) and V(t).
+      auto body = [&](auto A0, auto A1) {
+        constexpr bool kA0 = decltype(A0)::value, kA1 = decltype(A1)::value;
+        // distinct addresses per body: reads common to two bodies would be
+        // hoisted above the branch, all live at once
+        asm volatile("" : "+v"(qa.addr), "+v"(pva.addr));
+        bf16x8 pb[4];
+        if constexpr (kA1) {
+          qk_tile(qa, kso, qf, nx0, nx1);
+        } else {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) nx0[v] = nx1[v] = -INFINITY;
+        }
+        if constexpr (kA0) softmax_exp(cur0, cur1, c, exp_base(rs), pb, rs.lsum);
+        if constexpr (kA0 && kA1) {
+          interleave_qk_exp();
+          // P(t) and l are complete here: otherwise the exponentials sink
+          // past the mask branch, away from the MFMAs they overlap
+          asm volatile("" : "+v"(pb[0]), "+v"(pb[1]), "+v"(pb[2]), "+v"(pb[3]), "+v"(rs.lsum));
+        }
+        if constexpr (!kA0 && kA1) pace_qk();
+        if constexpr (kA1) {
+          if (!a1 || needs_mask(c1, wave)) mask_tile(nx0, nx1, c1, wave, qrow, hf, !a1);
+        }
+        float mx = -INFINITY;
+        if constexpr (kA0) pv_tile(pva, vso, pb, rs);
+        if constexpr (kA1) mx = tile_max(nx0, nx1);
+        if constexpr (kA0 && kA1) interleave_pv_max();
+        if constexpr (kA1) rescale(rs, mx * c);
+      };
+      using T = std::true_type;
+      using F = std::false_type;
+      if (a0)
+        body(T{}, T{});
+      else if (a1)
+        body(F{}, T{});
+      else
+        body(F{}, F{});
+      wait_dma();
+      __syncthreads();
+      c0 = c1;
+      c1 = c2;
+      c2 = make_step(raw3, t + 3 < nsteps);
+    };
+
+    for (int t = 0; t < nsteps; t += 2) {
+      step(t, 0, sa0, sa1, sb0, sb1);
+      if (t + 1 >= nsteps) break;
+      step(t + 1, 1, sb0, sb1, sa0, sa1);
+    }
   }
 
   // ---- epilogue: O = O^T / l, lane writes dims 32db + 8i + 4hf .. +3 of its row
