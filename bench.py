@@ -33,6 +33,24 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def measured_traffic():
+    """HBM bytes per attention launch from the committed rocprofv3 counter
+    summary (FETCH_SIZE and WRITE_SIZE, scaled by the copy-kernel factors), or
+    None when the attention kernel source has changed since it was taken."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", "attn_bf16_long64k_hbm_traffic.md")
+    src = os.path.join(ROOT, "paper_2606_09441_amd", "csrc", "attn_bf16.hip")
+    try:
+        text = open(path).read()
+        m = re.search(r"```json\s*(\{.*?\})\s*```", text, re.S)
+        info = json.loads(m.group(1))
+        digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    except (OSError, AttributeError, ValueError):
+        return None
+    return info["hbm_bytes_per_launch"] if info.get("source_sha256") == digest else None
+
+
 def tile_tables(seg_offsets, prompt_seg_ptr, tile):
     """Per global tile: token count and first tile of its prompt (segment-local tiling)."""
     lens, lo = [], []
@@ -259,7 +277,10 @@ def main():
             "peak": BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
-            "traffic": None,
+            # HBM bytes per launch (rocprofv3 counters), only for the long64k
+            # workload they were taken on
+            "traffic": measured_traffic() if args.workload == "long64k" and args.rho is None
+                       else None,
         },
         "cpu_baseline": cpu,
     }

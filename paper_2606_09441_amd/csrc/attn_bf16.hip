@@ -90,16 +90,17 @@ __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
 }
 
 // One step of a unit's merged list (see WorkTables), wave-uniform.
+// Wavefronts 0-1 own the unit's first M-block, 2-3 its second.
 struct Step {
   int tok0;  // first token of the key tile
-  int info;  // len | in0 | in1 | diag0 | diag1
+  int info;  // len | listed << 8 | diagonal << 12
   bool valid;
   __device__ __forceinline__ int len() const { return info & kStepLenMask; }
   __device__ __forceinline__ bool in(int w) const {
-    return (info & (w < 2 ? kStepIn0 : kStepIn1)) != 0;
+    return (info >> (kStepListedShift + (w >> 1))) & 1;
   }
   __device__ __forceinline__ bool diag(int w) const {
-    return (info & (w < 2 ? kStepDiag0 : kStepDiag1)) != 0;
+    return (info >> (kStepDiagShift + (w >> 1))) & 1;
   }
 };
 
@@ -107,6 +108,9 @@ __device__ __forceinline__ Step make_step(int2 x, bool valid) {
   Step s;
   s.tok0 = __builtin_amdgcn_readfirstlane(x.x);
   s.info = __builtin_amdgcn_readfirstlane(x.y);
+  // decoded here, not where first used: sunk into the next step, the wait
+  // for x would also wait for that step's DMA
+  asm volatile("" : "+s"(s.tok0), "+s"(s.info));
   s.valid = valid;
   if (!valid) s.info = kT;  // a full-length dummy for unconditional reloads
   return s;
@@ -205,7 +209,7 @@ __device__ __forceinline__ void qk_tile(const QkArgs& q, int slot_off, const bf1
 __device__ __forceinline__ void swap_halves(float x, float& a, float& b) {
   a = x;
   b = x;
-  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+  asm("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
 }
 
 __device__ __forceinline__ float swap_max(float x) {
@@ -355,7 +359,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
   if (unit < 0) return;
   const int h = wt.unit_head[unit];
   const int m0 = wt.unit_m0[unit];
-  const int m1 = wt.unit_m1[unit];
+  const int m1 = wt.unit_nb[unit] > 1 ? m0 + 1 : -1;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform

@@ -11,15 +11,16 @@
 //                 tile of the prompt up to the row's own (Section 5.1: query
 //                 M-blocks count all causal N-blocks).
 //   decode_scan   exclusive prefix sum of the counts -> row_ptr (one block).
-//   decode_write  one wavefront per attention work unit (query head, M-blocks
-//                 m0 and m0+1 of one segment): CA pages of the earlier
-//                 documents in document order, then LA tiles, then the
-//                 diagonals; each chunk of 64 bits becomes indices through a
-//                 ballot and a lane-prefix popcount, so every output is dense
-//                 and in ascending global tile order.  It writes both rows'
-//                 lists and the unit's merged step list (the union of the two
-//                 lists, each step flagged with the M-blocks that list it),
-//                 which the attention kernel streams.
+//   decode_write  one wavefront per attention work unit (query head, up to
+//                 four consecutive M-blocks of one segment): CA pages of the
+//                 earlier documents in document order, then the LA tiles
+//                 (diagonals included); each chunk of 64 candidate tiles
+//                 becomes indices through a ballot and a lane-prefix
+//                 popcount, so every output is dense and in ascending global
+//                 tile order.  It writes every row's list and the unit's
+//                 merged step list (the union of the rows' lists, each step
+//                 flagged with the M-blocks that list it), which the
+//                 attention kernel streams.
 // Bits are most significant first inside each byte (Section 4.1).
 
 #include "sift_internal.h"
@@ -112,31 +113,34 @@ __global__ __launch_bounds__(1024) void decode_scan(const int32_t* __restrict__ 
 }
 
 // Wave-cooperative emitter of one unit's outputs.  Each call handles up to 64
-// candidate key tiles n (one per lane): `a` marks those m0 lists, `b` those
-// m1 lists; they are appended, in lane order, to m0's list, m1's list and the
-// merged step list.
+// candidate key tiles n (one per lane); bit k of `listed` says M-block m0 + k
+// lists n.  Tiles are appended, in lane order, to the lists of the M-blocks
+// that list them and, once, to the merged step list.
 struct Emitter {
   int32_t* col;
   int2* steps;
   const PlanTables* pt;
-  int32_t p0, p1, ps;  // next write positions (m0 list, m1 list, steps)
-  int32_t m0, m1;
-  int lane;
+  int32_t pos[kUnitBlocks];  // next write position in each M-block's list
+  int32_t ps;                // next write position in the step list
+  int32_t m0, nb;
   unsigned long long below;
 
-  __device__ __forceinline__ void emit(bool a, bool b, int32_t n) {
-    const unsigned long long ma = __ballot(a);
-    const unsigned long long mb = __ballot(b);
-    const unsigned long long mu = __ballot(a || b);
-    if (a) col[p0 + __popcll(ma & below)] = n;
-    if (b) col[p1 + __popcll(mb & below)] = n;
-    if (a || b) {
-      const int info = pt->tile_len[n] | (a ? kStepIn0 : 0) | (b ? kStepIn1 : 0) |
-                       (n == m0 ? kStepDiag0 : 0) | (n == m1 ? kStepDiag1 : 0);
+  __device__ __forceinline__ void emit(unsigned listed, int32_t n) {
+#pragma unroll
+    for (int k = 0; k < kUnitBlocks; ++k) {
+      if (k >= nb) break;
+      const bool on = (listed >> k) & 1u;
+      const unsigned long long mk = __ballot(on);
+      if (on) col[pos[k] + __popcll(mk & below)] = n;
+      pos[k] += __popcll(mk);
+    }
+    const unsigned long long mu = __ballot(listed != 0u);
+    if (listed != 0u) {
+      const unsigned diag = (n >= m0 && n < m0 + nb) ? 1u << (n - m0) : 0u;
+      const int info = pt->tile_len[n] | static_cast<int>(listed << kStepListedShift) |
+                       static_cast<int>(diag << kStepDiagShift);
       steps[ps + __popcll(mu & below)] = make_int2(pt->tile_tok0[n], info);
     }
-    p0 += __popcll(ma);
-    p1 += __popcll(mb);
     ps += __popcll(mu);
   }
 };
@@ -151,60 +155,63 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   if (u >= wt.num_units) return;  // uniform per wavefront
   const int h = wt.unit_head[u];
   const int m0 = wt.unit_m0[u];
-  const int m1 = wt.unit_m1[u];
-  const bool two = m1 >= 0;
+  const int nb = wt.unit_nb[u];
+  const unsigned all = (1u << nb) - 1u;
   const int64_t r0 = static_cast<int64_t>(h) * pt.num_tiles + m0;
   Emitter e;
   e.col = col;
   e.steps = wt.steps;
   e.pt = &pt;
-  e.p0 = row_ptr[r0];
-  e.p1 = two ? row_ptr[r0 + 1] : 0;
+#pragma unroll
+  for (int k = 0; k < kUnitBlocks; ++k) e.pos[k] = k < nb ? row_ptr[r0 + k] : 0;
   e.ps = wt.step_off[u];
   e.m0 = m0;
-  e.m1 = m1;
-  e.lane = lane;
+  e.nb = nb;
   e.below = (1ull << lane) - 1ull;
   const int s = pt.tile_seg[m0];
+  const int mlast = m0 + nb - 1;
   if (pt.seg_kind[s] == kQuery) {
-    // every tile of the prompt up to the M-block (Section 5.1)
+    // every tile of the prompt up to the M-block (Section 5.1): M-block m0 +
+    // k lists n when n <= m0 + k
     const int lo = pt.tile_lo[m0];
-    for (int k0 = lo; k0 <= m0; k0 += 64) {
+    for (int k0 = lo; k0 <= mlast; k0 += 64) {
       const int n = k0 + lane;
-      const bool ok = n <= m0;
-      e.emit(ok, ok && two, n);
+      unsigned listed = 0u;
+      if (n <= mlast) listed = n < m0 ? all : (all & ~((1u << (n - m0)) - 1u));
+      e.emit(listed, n);
     }
   } else {
-    // CA pages of every earlier document: shared by both M-blocks
+    // CA pages of every earlier document: the same for all M-blocks
     for (int d = pt.seg_first[s]; d < s; ++d) {
       const int Pe = pt.seg_pages[d];
       const uint8_t* cav = ca + pt.seg_ca_off[d] + static_cast<int64_t>(h) * ca_nbytes(Pe);
       for (int c0 = 0; c0 < Pe; c0 += 64) {
         const int b = c0 + lane;
         const bool on = b < Pe && get_bit(cav, b);
-        e.emit(on, on && two, pt.seg_tile0[d] + b);
+        e.emit(on ? all : 0u, pt.seg_tile0[d] + b);
       }
     }
-    // LA row i (m0) and row i+1 (m1), tiles j = 0..i; j == i is m0's diagonal
+    // LA rows i .. i+nb-1 of the document's triangle, tiles j = 0 .. i+nb-1;
+    // row r lists j < r when its bit is set, and its diagonal j == r
     const int i = m0 - pt.seg_tile0[s];
     const int P = pt.seg_pages[s];
     const uint8_t* lav = la + pt.seg_la_off[s] + static_cast<int64_t>(h) * la_nbytes(P);
-    const int row_a = i * (i + 1) / 2;
-    const int row_b = (i + 1) * (i + 2) / 2;
-    for (int c0 = 0; c0 <= i; c0 += 64) {
+    for (int c0 = 0; c0 < i + nb; c0 += 64) {
       const int j = c0 + lane;
-      const bool in = j <= i;
-      const bool a = in && (j == i || get_bit(lav, row_a + j));
-      const bool b = in && two && get_bit(lav, row_b + j);
-      e.emit(a, b, pt.seg_tile0[s] + j);
+      unsigned listed = 0u;
+#pragma unroll
+      for (int k = 0; k < kUnitBlocks; ++k) {
+        const int r = i + k;
+        if (k < nb && j <= r && (j == r || get_bit(lav, r * (r + 1) / 2 + j))) listed |= 1u << k;
+      }
+      e.emit(listed, pt.seg_tile0[s] + j);
     }
   }
-  if (two) e.emit(false, lane == 0, m1);  // m1's diagonal
   if (lane == 0) wt.step_cnt[u] = e.ps - wt.step_off[u];
 }
 
 // Generic merge of caller-given lists (one thread per unit): the union of
-// rows m0 and m1, ascending, entries outside [first tile of the prompt,
+// the unit's rows, ascending, entries outside [first tile of the prompt,
 // M-block] skipped, at most step_off[u+1] - step_off[u] steps.
 __global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
                                                    const int32_t* __restrict__ row_ptr,
@@ -214,39 +221,50 @@ __global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
   if (u >= wt.num_units) return;
   const int h = wt.unit_head[u];
   const int m0 = wt.unit_m0[u];
-  const int m1 = wt.unit_m1[u];
+  const int nb = wt.unit_nb[u];
   const int lo = pt.tile_lo[m0];
   const int64_t r0 = static_cast<int64_t>(h) * pt.num_tiles + m0;
   auto clampi = [cap](int64_t x) { return min(cap, max(static_cast<int64_t>(0), x)); };
-  int64_t ia = clampi(row_ptr[r0]);
-  const int64_t ea = max(ia, clampi(row_ptr[r0 + 1]));
-  int64_t ib = 0, eb = 0;
-  if (m1 >= 0) {
-    ib = clampi(row_ptr[r0 + 1]);
-    eb = max(ib, clampi(row_ptr[r0 + 2]));
+  int64_t it[kUnitBlocks], end[kUnitBlocks];
+#pragma unroll
+  for (int k = 0; k < kUnitBlocks; ++k) {
+    it[k] = 0;
+    end[k] = 0;
+    if (k < nb) {
+      it[k] = clampi(row_ptr[r0 + k]);
+      end[k] = max(it[k], clampi(row_ptr[r0 + k + 1]));
+    }
   }
   const int base = wt.step_off[u];
   const int room = wt.step_off[u + 1] - base;
   int ns = 0;
   while (ns < room) {
-    int na = 0x7fffffff, nb = 0x7fffffff;
-    while (ia < ea) {
-      const int n = col[ia];
-      if (n >= lo && n <= m0) { na = n; break; }
-      ++ia;
+    int head[kUnitBlocks];
+    int n = 0x7fffffff;
+#pragma unroll
+    for (int k = 0; k < kUnitBlocks; ++k) {
+      head[k] = 0x7fffffff;
+      while (it[k] < end[k]) {
+        const int x = col[it[k]];
+        if (x >= lo && x <= m0 + k) {
+          head[k] = x;
+          break;
+        }
+        ++it[k];
+      }
+      n = min(n, head[k]);
     }
-    while (ib < eb) {
-      const int n = col[ib];
-      if (n >= lo && n <= m1) { nb = n; break; }
-      ++ib;
-    }
-    const int n = min(na, nb);
     if (n == 0x7fffffff) break;
-    const bool a = na == n, b = nb == n;
-    if (a) ++ia;
-    if (b) ++ib;
-    const int info = pt.tile_len[n] | (a ? kStepIn0 : 0) | (b ? kStepIn1 : 0) |
-                     (n == m0 ? kStepDiag0 : 0) | (n == m1 ? kStepDiag1 : 0);
+    unsigned listed = 0u;
+#pragma unroll
+    for (int k = 0; k < kUnitBlocks; ++k)
+      if (head[k] == n) {
+        listed |= 1u << k;
+        ++it[k];
+      }
+    const unsigned diag = (n >= m0 && n < m0 + nb) ? 1u << (n - m0) : 0u;
+    const int info = pt.tile_len[n] | static_cast<int>(listed << kStepListedShift) |
+                     static_cast<int>(diag << kStepDiagShift);
     wt.steps[base + ns] = make_int2(pt.tile_tok0[n], info);
     ++ns;
   }

@@ -80,7 +80,7 @@ sift_status check_io(const sift_tensor* q, const sift_tensor* k, const sift_tens
 struct HostPlan {
   std::vector<int32_t> seg_tile0, seg_pages, seg_kind, seg_first, seg_la_off, seg_ca_off;
   std::vector<int32_t> tile_seg, tile_tok0, tile_len, tile_lo;
-  std::vector<int32_t> unit_head, unit_m0, unit_m1, sched, step_off;
+  std::vector<int32_t> unit_head, unit_m0, unit_nb, sched, step_off;
   int64_t dense_tiles = 0;  // causal tiles of all prompts, one head
   int64_t la_bytes = 0, ca_bytes = 0;
   int32_t num_tokens = 0, num_segments = 0, num_tiles = 0;
@@ -158,52 +158,55 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
     }
   }
 
-  // Attention work units: (query head, M-blocks 2p and 2p+1 of a segment).
-  struct Pair {
-    int32_t m0, m1;
-    int64_t cost;  // causal tiles of the pair's later M-block: the list-length bound
+  // Attention work units: (query head, M-blocks kUnitBlocks*p .. of a
+  // segment).  The M-blocks of one document share the cross-attention part
+  // of their lists (it depends on the key document only), so a unit stages
+  // each of those key tiles once for all of its query rows.
+  struct Group {
+    int32_t m0, nb;
+    int64_t cost;  // causal tiles of the group's last M-block: the union's length bound
   };
-  std::vector<Pair> pairs;
+  std::vector<Group> groups;
   for (int32_t s = 0; s < S; ++s) {
     const int32_t lo = hp.seg_tile0[hp.seg_first[s]];  // first tile of the prompt
-    for (int32_t p = 0; p < hp.seg_pages[s]; p += 2) {
+    for (int32_t p = 0; p < hp.seg_pages[s]; p += sift::kUnitBlocks) {
       const int32_t m0 = hp.seg_tile0[s] + p;
-      const int32_t m1 = p + 1 < hp.seg_pages[s] ? m0 + 1 : -1;
-      pairs.push_back({m0, m1, (m1 >= 0 ? m1 : m0) - lo + 1});
+      const int32_t nb = std::min<int32_t>(sift::kUnitBlocks, hp.seg_pages[s] - p);
+      groups.push_back({m0, nb, m0 + nb - 1 - lo + 1});
     }
   }
-  // Units in locality order: kv head, then longest pair first, then the query
-  // heads of the group side by side (they read the same key tiles).
+  // Units in locality order: kv head, then longest group first, then the
+  // query heads of the kv group side by side (they read the same key tiles).
   const int32_t g = hq / hkv;
-  std::vector<int32_t> pord(pairs.size());
-  std::iota(pord.begin(), pord.end(), 0);
-  std::stable_sort(pord.begin(), pord.end(),
-                   [&](int32_t x, int32_t y) { return pairs[x].cost > pairs[y].cost; });
-  const int64_t U = static_cast<int64_t>(pairs.size()) * hq;
+  std::vector<int32_t> gord(groups.size());
+  std::iota(gord.begin(), gord.end(), 0);
+  std::stable_sort(gord.begin(), gord.end(),
+                   [&](int32_t x, int32_t y) { return groups[x].cost > groups[y].cost; });
+  const int64_t U = static_cast<int64_t>(groups.size()) * hq;
   if (U > i32max / 2) return SIFT_E_CAPACITY;
   std::vector<int32_t> order;  // unit ids
   order.reserve(U);
   hp.unit_head.resize(U);
   hp.unit_m0.resize(U);
-  hp.unit_m1.resize(U);
+  hp.unit_nb.resize(U);
   std::vector<int64_t> unit_cost(U);
   int32_t u = 0;
   for (int32_t kv = 0; kv < hkv; ++kv)
-    for (int32_t pi : pord)
+    for (int32_t gi : gord)
       for (int32_t j = 0; j < g; ++j) {
         hp.unit_head[u] = kv * g + j;
-        hp.unit_m0[u] = pairs[pi].m0;
-        hp.unit_m1[u] = pairs[pi].m1;
-        unit_cost[u] = pairs[pi].cost;
+        hp.unit_m0[u] = groups[gi].m0;
+        hp.unit_nb[u] = groups[gi].nb;
+        unit_cost[u] = groups[gi].cost;
         order.push_back(u);
         ++u;
       }
-  // Each unit's merged step list has room for both M-blocks' causal tiles.
+  // A unit's merged list is a subset of the tiles from the prompt's first
+  // to its last M-block.
   hp.step_off.assign(U + 1, 0);
   for (int64_t k = 0; k < U; ++k) {
-    const int32_t m0 = hp.unit_m0[k], m1 = hp.unit_m1[k];
-    const int32_t lo = hp.tile_lo[m0];
-    hp.step_off[k + 1] = hp.step_off[k] + (m0 - lo + 1) + (m1 >= 0 ? m1 - lo + 1 : 0);
+    if (hp.step_off[k] + unit_cost[k] > i32max) return SIFT_E_CAPACITY;
+    hp.step_off[k + 1] = hp.step_off[k] + static_cast<int32_t>(unit_cost[k]);
   }
   // Split the locality order into kNumXcd contiguous chunks; workgroup
   // x + kNumXcd * k runs chunk x's k-th unit (longest first inside a chunk).
@@ -274,7 +277,7 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   const size_t o_sched = put(blob, hp.sched);
   const size_t o_uh = put(blob, hp.unit_head);
   const size_t o_um0 = put(blob, hp.unit_m0);
-  const size_t o_um1 = put(blob, hp.unit_m1);
+  const size_t o_unb = put(blob, hp.unit_nb);
   const size_t o_soff = put(blob, hp.step_off);
   const int64_t rows = static_cast<int64_t>(hp.num_tiles) * num_q_heads;
   const int64_t cap = hp.dense_tiles * num_q_heads;
@@ -323,7 +326,7 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   plan->wt.sched = P(o_sched);
   plan->wt.unit_head = P(o_uh);
   plan->wt.unit_m0 = P(o_um0);
-  plan->wt.unit_m1 = P(o_um1);
+  plan->wt.unit_nb = P(o_unb);
   plan->wt.step_off = P(o_soff);
   plan->wt.step_cnt = P(o_scnt);
   plan->wt.steps = reinterpret_cast<int2*>(P(o_steps));

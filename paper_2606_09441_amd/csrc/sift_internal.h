@@ -27,18 +27,21 @@ struct PlanTables {
   int32_t num_q_heads;        // Hq
 };
 
-// Attention work: one unit = (query head, a pair of consecutive M-blocks of
-// one segment).  sched[g] is the unit run by workgroup g, or -1 for none.
-// A unit's merged step list (the union of its two M-blocks' lists, in
-// ascending key-tile order) lives at steps[step_off[u] ..
-// step_off[u] + step_cnt[u]); step_off[u+1] - step_off[u] bounds its length.
-// Step = {first token of the key tile, len | in0 << 8 | in1 << 9 |
-// (n == m0) << 10 | (n == m1) << 11}.
+// Attention work: one unit = (query head, up to kUnitBlocks consecutive
+// M-blocks of one segment).  sched[g] is the unit run by workgroup g, or -1
+// for none.  A unit's merged step list (the union of its M-blocks' lists, in
+// ascending key-tile order) lives at steps[step_off[u] .. step_off[u] +
+// step_cnt[u]); step_off[u+1] - step_off[u] bounds its length.
+// Step = {first token of the key tile, len | listed << 8 | diagonal << 12},
+// where bit k of `listed` says M-block m0 + k lists the tile and bit k of
+// `diagonal` says the tile is m0 + k itself.
+constexpr int kUnitBlocks = 2;
+
 struct WorkTables {
   const int32_t* sched;       // [grid]
   const int32_t* unit_head;   // [U]
   const int32_t* unit_m0;     // [U] first M-block
-  const int32_t* unit_m1;     // [U] second M-block, or -1
+  const int32_t* unit_nb;     // [U] M-blocks in the unit, 1 .. kUnitBlocks
   const int32_t* step_off;    // [U + 1]
   int32_t* step_cnt;          // [U] (device scratch)
   int2* steps;                // [step_off[U]] (device scratch)
@@ -47,13 +50,11 @@ struct WorkTables {
 };
 
 constexpr int kStepLenMask = 0xff;
-constexpr int kStepIn0 = 1 << 8;
-constexpr int kStepIn1 = 1 << 9;
-constexpr int kStepDiag0 = 1 << 10;
-constexpr int kStepDiag1 = 1 << 11;
+constexpr int kStepListedShift = 8;
+constexpr int kStepDiagShift = 12;
 
 // Decode (Section 5.1): count, scan, write.  The write pass runs per unit and
-// emits both M-blocks' lists and the unit's merged step list.
+// emits its M-blocks' lists and the unit's merged step list.
 hipError_t launch_decode(const PlanTables& pt, const WorkTables& wt, const uint8_t* la,
                          const uint8_t* ca, int32_t* counts, int32_t* row_ptr, int32_t* col_idx,
                          hipStream_t stream);
