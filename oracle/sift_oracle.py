@@ -32,14 +32,14 @@ What the oracle computes (paper: SIFT, arXiv 2606.09441):
 * The decoded list of a (head, M-block) holds every N-block the mask touches,
   in ascending order (Section 5.1, sparse_n_indices).
 
-Readings where the paper is silent (each one is listed in DESIGN.md): "head"
-means query head; the kv head of query head h is h // (Hq / Hkv); tiles are
+Readings taken where the paper is silent: "head" means query head; the kv head of query head h is h // (Hq / Hkv); tiles are
 segment local (a tile never straddles a document or the query, and the last
 tile of a segment may be partial); CA bits are MSB first by page index; the
 softmax scale is 1/sqrt(D); the bit-vector buffers concatenate, over prompts,
 documents in prompt order and query heads 0..Hq-1, each document's vector; the
 global number of tile i of segment s is the number of tiles in all earlier
-segments (of all prompts) plus i.
+segments (of all prompts) plus i; a document's rows see the CA-marked pages
+of every earlier document of the prompt.
 
 All inputs are taken at their exact values: bf16 or fp32 numbers are widened
 to float64 without rounding.
