@@ -10,7 +10,8 @@
 //                 every earlier document of the prompt.  Query rows: every
 //                 tile of the prompt up to the row's own (Section 5.1: query
 //                 M-blocks count all causal N-blocks).
-//   decode_scan   exclusive prefix sum of the counts -> row_ptr (one block).
+//   decode_scan   exclusive prefix sum of the counts -> row_ptr (one
+//                 workgroup, coalesced two-pass scan).
 //   decode_write  one wavefront per attention work unit (query head, up to
 //                 four consecutive M-blocks of one segment): CA pages of the
 //                 earlier documents in document order, then the LA tiles
@@ -77,39 +78,51 @@ __global__ __launch_bounds__(256) void decode_count(PlanTables pt, const uint8_t
 // Exclusive scan of n counts into row_ptr[0..n]; a single 1024-thread block.
 // Thread t owns a contiguous chunk; chunk totals are scanned with wavefront
 // shuffles and one LDS step across the 16 wavefronts.
+// Exclusive prefix sum of the counts in one workgroup of 16 wavefronts.
+// Wavefront w owns a chunk of consecutive rows (a multiple of 256 long).
+// Pass 1 sums the chunk with coalesced loads; the chunk offsets come from the
+// 16 totals in LDS.  Pass 2 walks the chunk 256 rows at a time, 4 per lane:
+// a lane-local prefix, a wavefront scan of the lane sums, coalesced stores.
 __global__ __launch_bounds__(1024) void decode_scan(const int32_t* __restrict__ counts,
                                                     int32_t* __restrict__ row_ptr, int64_t n) {
   __shared__ int32_t wsum[16];
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int w = t >> 6;
-  const int64_t per = (n + 1023) / 1024;
-  const int64_t a = min(n, static_cast<int64_t>(t) * per);
+  const int64_t per = ((n + 15) / 16 + 255) / 256 * 256;
+  const int64_t a = min(n, static_cast<int64_t>(w) * per);
   const int64_t z = min(n, a + per);
   int32_t s = 0;
-  for (int64_t i = a; i < z; ++i) s += counts[i];
-  int32_t x = s;  // inclusive scan inside the wavefront
-  for (int off = 1; off < 64; off <<= 1) {
-    const int32_t y = __shfl_up(x, off, 64);
-    if (lane >= off) x += y;
-  }
-  if (lane == 63) wsum[w] = x;
+  for (int64_t i = a + lane; i < z; i += 64) s += counts[i];
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+  if (lane == 0) wsum[w] = s;
   __syncthreads();
-  if (w == 0) {
-    int32_t ws = lane < 16 ? wsum[lane] : 0;
-    for (int off = 1; off < 16; off <<= 1) {
-      const int32_t y = __shfl_up(ws, off, 64);
-      if (lane >= off) ws += y;
+  int32_t base = 0;
+  for (int j = 0; j < w; ++j) base += wsum[j];
+  for (int64_t g = a; g < z; g += 256) {
+    const int64_t i0 = g + 4 * lane;
+    int32_t v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = i0 + k < z ? counts[i0 + k] : 0;
+    const int32_t own = v[0] + v[1] + v[2] + v[3];
+    int32_t x = own;  // inclusive scan of the lane sums
+    for (int off = 1; off < 64; off <<= 1) {
+      const int32_t y = __shfl_up(x, off, 64);
+      if (lane >= off) x += y;
     }
-    if (lane < 16) wsum[lane] = ws;
+    int32_t e = base + x - own;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (i0 + k < z) row_ptr[i0 + k] = e;
+      e += v[k];
+    }
+    base += __shfl(x, 63, 64);
   }
-  __syncthreads();
-  int32_t excl = x - s + (w > 0 ? wsum[w - 1] : 0);
-  for (int64_t i = a; i < z; ++i) {
-    row_ptr[i] = excl;
-    excl += counts[i];
+  if (t == 0) {
+    int32_t total = 0;
+    for (int j = 0; j < 16; ++j) total += wsum[j];
+    row_ptr[n] = total;
   }
-  if (t == 1023) row_ptr[n] = excl;
 }
 
 // Wave-cooperative emitter of one unit's outputs.  Each call handles up to 64
