@@ -95,6 +95,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--paged", action="store_true",
+                    help="also time the step with K/V in a page pool (random page order)")
     ap.add_argument("--only-steps", action="store_true",
                     help="run warmup + timed steps only (for profiler runs)")
     args = ap.parse_args()
@@ -208,6 +210,29 @@ def main():
             f"({flops_d / ms_attn_d / 1e9:.1f} TFLOP/s); speedup {ms_step_d / ms_step:.2f}x "
             f"vs 1/density {1 / density:.2f}")
 
+    paged = None
+    if args.paged:
+        # K/V in a pool of T-row pages, one page per tile, in a random order
+        tl = torch.from_numpy(tlen).to(dev)
+        T = wl.tile
+        perm = np.random.default_rng(1).permutation(M).astype(np.int32)
+        kp = torch.zeros((M * T, wl.hkv, wl.d), dtype=dt, device=dev)
+        vp = torch.zeros_like(kp)
+        tok0 = np.concatenate([[0], np.cumsum(tlen)[:-1]]).astype(np.int64)
+        for m in range(M):
+            p, a, n = int(perm[m]), int(tok0[m]), int(tlen[m])
+            kp[p * T: p * T + n] = k[a: a + n]
+            vp[p * T: p * T + n] = v[a: a + n]
+        table = torch.from_numpy(perm).to(dev)
+        step_p = lambda: plan.run_paged(q, kp, vp, table, la, ca, out=out)
+        for _ in range(args.warmup):
+            step_p()
+        ms_step_p = timed(step_p, args.steps)
+        paged = {"ms_per_step": round(ms_step_p, 4),
+                 "useful_tflops_step": round(flops / ms_step_p / 1e9, 2)}
+        log(f"paged K/V: step {ms_step_p:.3f} ms ({flops / ms_step_p / 1e9:.1f} TFLOP/s)")
+        del kp, vp, tl
+
     cpu = None
     if not args.no_cpu_baseline:
         from oracle import sift_oracle as O
@@ -271,6 +296,7 @@ def main():
         "plan_ms": round(plan_ms, 3),
         "pct_bf16_peak_attention": round(100 * achieved / BF16_PEAK_TFLOPS, 2),
         "dense": dense or None,
+        "paged": paged,
         "roofline": {
             "bound": "mfma",
             "achieved": round(achieved, 2),

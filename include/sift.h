@@ -168,7 +168,9 @@ sift_status sift_plan_decode(sift_plan* plan, const uint8_t* local_bitmap,
  * Sparse attention (Section 5.2) over the lists the last sift_plan_decode
  * (or sift_plan_run, or sift_decode_tiles) on this plan produced: the
  * second step of sift_plan_run.  Tensors, scale and output as in
- * sift_sparse_attention.
+ * sift_sparse_attention.  SIFT_E_PLAN (bf16 inputs) when the last decode on
+ * the plan was the one of sift_plan_run_paged: its step lists index a page
+ * pool; decode again first.
  */
 sift_status sift_plan_attention(sift_plan* plan, const sift_tensor* q, const sift_tensor* k,
                                 const sift_tensor* v, float softmax_scale, sift_tensor* out,
@@ -206,6 +208,31 @@ sift_status sift_plan_run(sift_plan* plan, const sift_tensor* q,
                           const uint8_t* local_bitmap,
                           const uint8_t* cross_bitmap, float softmax_scale,
                           sift_tensor* out, void* stream);
+
+/*
+ * sift_plan_run with K and V in a page pool instead of packed on the token
+ * axis.  The paper's key tiles are KV pages (Sections 4.2-4.3): here a tile
+ * is one page of T rows, and page_table says where each tile lives.
+ *   k_pages, v_pages  device tensors [num_pages * T][Hkv][D] (tokens =
+ *                num_pages * T, a multiple of T, >= T when the layout has
+ *                tiles): page p holds rows p*T .. p*T + T-1, each row the
+ *                Hkv x D values of one token.  A partial last tile of a
+ *                segment uses the first tile_len rows of its page; the rest
+ *                of the page is never read.
+ *   page_table   device int32 [num_tiles]: page_table[m] = pool page of
+ *                global tile m (tile numbering as in "Tiles" above).  Entries
+ *                outside [0, num_pages) are clamped into the pool (no access
+ *                leaves it; the result for such tiles is meaningless).
+ *   q, out       packed as everywhere else; dtypes as in sift_sparse_attention.
+ * The plan's step lists then index the pool (see sift_plan_attention).
+ * Errors: those of sift_plan_run; SIFT_E_SHAPE for a pool that is not whole
+ * pages of the plan's T, Hkv, D; SIFT_E_NULL for a missing page_table.
+ */
+sift_status sift_plan_run_paged(sift_plan* plan, const sift_tensor* q,
+                                const sift_tensor* k_pages, const sift_tensor* v_pages,
+                                const int32_t* page_table, const uint8_t* local_bitmap,
+                                const uint8_t* cross_bitmap, float softmax_scale,
+                                sift_tensor* out, void* stream);
 
 /*
  * One-shot form with the arguments of the paper's problem statement: Q, K,

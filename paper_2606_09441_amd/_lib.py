@@ -69,6 +69,9 @@ _SIGS = {
     "sift_plan_run": (ctypes.c_int, [_P, ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftTensor),
                                      ctypes.POINTER(SiftTensor), _P, _P, ctypes.c_float,
                                      ctypes.POINTER(SiftTensor), _P]),
+    "sift_plan_run_paged": (ctypes.c_int, [_P, ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftTensor),
+                                           ctypes.POINTER(SiftTensor), _P, _P, _P, ctypes.c_float,
+                                           ctypes.POINTER(SiftTensor), _P]),
     "sift_sparse_prefill": (ctypes.c_int, [ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftTensor),
                                            ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftLayout),
                                            _P, _P, ctypes.c_int32, ctypes.POINTER(SiftTensor), _P]),
@@ -232,6 +235,20 @@ class Plan:
         check("sift_plan_run", lib().sift_plan_run(
             self._h, ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), _ptr(la), _ptr(ca),
             ctypes.c_float(0.0 if scale is None else scale), ctypes.byref(od), _stream_ptr(stream)))
+        return out
+
+    def run_paged(self, q, k_pages, v_pages, page_table, la, ca, scale=None, out=None,
+                  out_dtype=None, stream=None):
+        """Decode + attention with K/V in a page pool (sift_plan_run_paged):
+        k_pages/v_pages [num_pages * T, Hkv, D], page_table int32 [num_tiles]."""
+        torch = _torch()
+        if out is None:
+            out = torch.empty(q.shape, dtype=out_dtype or q.dtype, device=q.device)
+        qd, kd, vd, od = tensor_desc(q), tensor_desc(k_pages), tensor_desc(v_pages), tensor_desc(out)
+        check("sift_plan_run_paged", lib().sift_plan_run_paged(
+            self._h, ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), _ptr(page_table),
+            _ptr(la), _ptr(ca), ctypes.c_float(0.0 if scale is None else scale), ctypes.byref(od),
+            _stream_ptr(stream)))
         return out
 
 

@@ -67,7 +67,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(PlanTables pt, AttnArgs a
   for (int64_t idx = beg; idx < end; ++idx) {
     const int n = a.col_idx[idx];
     if (n < lo || n > m) continue;  // outside the prompt or after the M-block
-    const int ktok0 = pt.tile_tok0[n];
+    const int ktok0 = kv_row0(pt, a.pages, n);
     const int klen = pt.tile_len[n];
     __syncthreads();  // previous tile fully consumed (and Qs written)
     for (int e = tid; e < T * D; e += 256) {

@@ -133,6 +133,7 @@ struct Emitter {
   int32_t* col;
   int2* steps;
   const PlanTables* pt;
+  KvPages pages;
   int32_t pos[kUnitBlocks];  // next write position in each M-block's list
   int32_t ps;                // next write position in the step list
   int32_t m0, nb;
@@ -152,7 +153,7 @@ struct Emitter {
       const unsigned diag = (n >= m0 && n < m0 + nb) ? 1u << (n - m0) : 0u;
       const int info = pt->tile_len[n] | static_cast<int>(listed << kStepListedShift) |
                        static_cast<int>(diag << kStepDiagShift);
-      steps[ps + __popcll(mu & below)] = make_int2(pt->tile_tok0[n], info);
+      steps[ps + __popcll(mu & below)] = make_int2(kv_row0(*pt, pages, n), info);
     }
     ps += __popcll(mu);
   }
@@ -162,7 +163,7 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
                                                     const uint8_t* __restrict__ la,
                                                     const uint8_t* __restrict__ ca,
                                                     const int32_t* __restrict__ row_ptr,
-                                                    int32_t* __restrict__ col) {
+                                                    int32_t* __restrict__ col, KvPages pages) {
   const int lane = threadIdx.x & 63;
   const int u = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (u >= wt.num_units) return;  // uniform per wavefront
@@ -175,6 +176,7 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   e.col = col;
   e.steps = wt.steps;
   e.pt = &pt;
+  e.pages = pages;
 #pragma unroll
   for (int k = 0; k < kUnitBlocks; ++k) e.pos[k] = k < nb ? row_ptr[r0 + k] : 0;
   e.ps = wt.step_off[u];
@@ -288,7 +290,7 @@ __global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
 
 hipError_t launch_decode(const PlanTables& pt, const WorkTables& wt, const uint8_t* la,
                          const uint8_t* ca, int32_t* counts, int32_t* row_ptr, int32_t* col_idx,
-                         hipStream_t stream) {
+                         const KvPages& pages, hipStream_t stream) {
   const int64_t rows = static_cast<int64_t>(pt.num_tiles) * pt.num_q_heads;
   if (rows == 0) {  // empty layout: the scan alone writes row_ptr[0] = 0
     hipLaunchKernelGGL(decode_scan, dim3(1), dim3(1024), 0, stream, counts, row_ptr, rows);
@@ -303,7 +305,7 @@ hipError_t launch_decode(const PlanTables& pt, const WorkTables& wt, const uint8
   if (e != hipSuccess) return e;
   if (wt.num_units == 0) return hipSuccess;
   hipLaunchKernelGGL(decode_write, dim3(static_cast<unsigned>((wt.num_units + 3) / 4)), dim3(256),
-                     0, stream, pt, wt, la, ca, row_ptr, col_idx);
+                     0, stream, pt, wt, la, ca, row_ptr, col_idx, pages);
   return hipGetLastError();
 }
 

@@ -37,6 +37,7 @@ struct sift_plan {
   int32_t* counts = nullptr;   // [num_rows]
   int32_t* row_ptr = nullptr;  // [num_rows + 1]
   int32_t* col_idx = nullptr;  // [list_capacity]
+  bool steps_paged = false;    // the last decode wrote page-pool rows into the steps
 };
 
 namespace {
@@ -321,6 +322,7 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   plan->pt.tile_tok0 = P(o_tile_tok0);
   plan->pt.tile_len = P(o_tile_len);
   plan->pt.tile_lo = P(o_tile_lo);
+  plan->pt.tile = tile;
   plan->pt.num_tiles = hp.num_tiles;
   plan->pt.num_q_heads = num_q_heads;
   plan->wt.sched = P(o_sched);
@@ -383,8 +385,11 @@ sift_status sift_decode_tiles(sift_plan* plan, const uint8_t* local_bitmap,
   if (st != SIFT_OK) return st;
   const hipError_t e = sift::launch_decode(plan->pt, work(plan), local_bitmap, cross_bitmap,
                                            plan->counts, row_ptr, col_idx,
+                                           sift::KvPages{nullptr, 0},
                                            static_cast<hipStream_t>(stream));
-  return e == hipSuccess ? SIFT_OK : SIFT_E_HIP;
+  if (e != hipSuccess) return SIFT_E_HIP;
+  plan->steps_paged = false;
+  return SIFT_OK;
 }
 
 sift_status sift_plan_decode(sift_plan* plan, const uint8_t* local_bitmap,
@@ -428,6 +433,7 @@ sift_status sift_sparse_attention(sift_plan* plan, const sift_tensor* q, const s
   if (bf16) {
     // the bf16 kernel walks merged per-unit step lists: build them from the lists
     e = sift::launch_merge_steps(plan->pt, work(plan), row_ptr, col_idx, col_capacity, s);
+    if (e == hipSuccess) plan->steps_paged = false;
     if (e == hipSuccess) e = sift::launch_attn_bf16(plan->pt, work(plan), a, s);
   } else {
     e = sift::launch_attn_f32(plan->pt, a, s);
@@ -443,6 +449,7 @@ sift_status sift_plan_attention(sift_plan* plan, const sift_tensor* q, const sif
   sift_status st = check_io(q, k, v, out, in.num_tokens, in.num_q_heads, in.num_kv_heads,
                             in.head_dim, in.tile);
   if (st != SIFT_OK) return st;
+  if (plan->steps_paged && q->dtype == SIFT_BF16) return SIFT_E_PLAN;  // steps index a page pool
   if ((st = check_device(plan)) != SIFT_OK) return st;
   if (!(softmax_scale > 0.f) || !std::isfinite(softmax_scale))
     softmax_scale = 1.0f / std::sqrt(static_cast<float>(in.head_dim));
@@ -481,6 +488,58 @@ sift_status sift_plan_run(sift_plan* plan, const sift_tensor* q, const sift_tens
   st = sift_plan_decode(plan, local_bitmap, cross_bitmap, stream);
   if (st != SIFT_OK) return st;
   return sift_plan_attention(plan, q, k, v, softmax_scale, out, stream);
+}
+
+
+sift_status sift_plan_run_paged(sift_plan* plan, const sift_tensor* q, const sift_tensor* k_pages,
+                                const sift_tensor* v_pages, const int32_t* page_table,
+                                const uint8_t* local_bitmap, const uint8_t* cross_bitmap,
+                                float softmax_scale, sift_tensor* out, void* stream) {
+  if (plan == nullptr || k_pages == nullptr || v_pages == nullptr) return SIFT_E_NULL;
+  const sift_plan_info& in = plan->info;
+  sift_status st;
+  if ((st = check_tensor(q, in.num_tokens, in.num_q_heads, in.head_dim)) != SIFT_OK) return st;
+  if ((st = check_tensor(out, in.num_tokens, in.num_q_heads, in.head_dim)) != SIFT_OK) return st;
+  // the pools: whole pages of T rows, at least one when there are tiles
+  const int32_t rows = k_pages->tokens;
+  if (rows < 0 || rows % in.tile != 0) return SIFT_E_SHAPE;
+  const int32_t num_pages = rows / in.tile;
+  if ((st = check_tensor(k_pages, rows, in.num_kv_heads, in.head_dim)) != SIFT_OK) return st;
+  if ((st = check_tensor(v_pages, rows, in.num_kv_heads, in.head_dim)) != SIFT_OK) return st;
+  if (in.num_tiles > 0 && num_pages < 1) return SIFT_E_SHAPE;
+  if (in.num_tiles > 0 && page_table == nullptr) return SIFT_E_NULL;
+  if (q->dtype != k_pages->dtype || q->dtype != v_pages->dtype) return SIFT_E_UNSUPPORTED;
+  if (q->dtype == SIFT_BF16 && (in.tile != 64 || in.head_dim != 128)) return SIFT_E_UNSUPPORTED;
+  if (q->dtype == SIFT_F32 && out->dtype != SIFT_F32) return SIFT_E_UNSUPPORTED;
+  if (in.la_bytes > 0 && local_bitmap == nullptr) return SIFT_E_NULL;
+  if (in.ca_bytes > 0 && cross_bitmap == nullptr) return SIFT_E_NULL;
+  if ((st = check_device(plan)) != SIFT_OK) return st;
+  if (!(softmax_scale > 0.f) || !std::isfinite(softmax_scale))
+    softmax_scale = 1.0f / std::sqrt(static_cast<float>(in.head_dim));
+  const sift::KvPages pages{page_table, num_pages};
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = sift::launch_decode(plan->pt, work(plan), local_bitmap, cross_bitmap,
+                                     plan->counts, plan->row_ptr, plan->col_idx, pages, s);
+  if (e != hipSuccess) return SIFT_E_HIP;
+  plan->steps_paged = true;
+  sift::AttnArgs a{};
+  a.q = q->data;
+  a.k = k_pages->data;
+  a.v = v_pages->data;
+  a.out = out->data;
+  a.row_ptr = plan->row_ptr;
+  a.col_idx = plan->col_idx;
+  a.col_capacity = in.list_capacity;
+  a.hq = in.num_q_heads;
+  a.hkv = in.num_kv_heads;
+  a.head_dim = in.head_dim;
+  a.tile = in.tile;
+  a.scale_log2 = softmax_scale * 1.4426950408889634f;
+  a.out_f32 = out->dtype == SIFT_F32 ? 1 : 0;
+  a.pages = pages;
+  e = q->dtype == SIFT_BF16 ? sift::launch_attn_bf16(plan->pt, work(plan), a, s)
+                            : sift::launch_attn_f32(plan->pt, a, s);
+  return e == hipSuccess ? SIFT_OK : SIFT_E_HIP;
 }
 
 sift_status sift_sparse_prefill(const sift_tensor* q, const sift_tensor* k, const sift_tensor* v,

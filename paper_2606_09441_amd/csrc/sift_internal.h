@@ -25,14 +25,31 @@ struct PlanTables {
   const int32_t* tile_lo;     // first tile of m's prompt
   int32_t num_tiles;          // M
   int32_t num_q_heads;        // Hq
+  int32_t tile;               // T
 };
+
+// Where the K/V rows of a key tile live.  Packed (table == nullptr): tile m
+// starts at token row tile_tok0[m] of k and v.  Paged: k and v are a pool of
+// num_pages pages of T rows each, and tile m is pool page table[m] (entries
+// outside [0, num_pages) are clamped into the pool, so no access leaves it).
+// Both layouts have the same row stride (Hkv * D elements).
+struct KvPages {
+  const int32_t* table;
+  int32_t num_pages;
+};
+
+__device__ __forceinline__ int32_t kv_row0(const PlanTables& pt, const KvPages& pg, int32_t m) {
+  if (pg.table == nullptr) return pt.tile_tok0[m];
+  const int32_t p = pg.table[m];
+  return (p < 0 ? 0 : (p >= pg.num_pages ? pg.num_pages - 1 : p)) * pt.tile;
+}
 
 // Attention work: one unit = (query head, up to kUnitBlocks consecutive
 // M-blocks of one segment).  sched[g] is the unit run by workgroup g, or -1
 // for none.  A unit's merged step list (the union of its M-blocks' lists, in
 // ascending key-tile order) lives at steps[step_off[u] .. step_off[u] +
 // step_cnt[u]); step_off[u+1] - step_off[u] bounds its length.
-// Step = {first token of the key tile, len | listed << 8 | diagonal << 12},
+// Step = {first K/V row of the key tile, len | listed << 8 | diagonal << 12},
 // where bit k of `listed` says M-block m0 + k lists the tile and bit k of
 // `diagonal` says the tile is m0 + k itself.
 constexpr int kUnitBlocks = 2;
@@ -57,7 +74,7 @@ constexpr int kStepDiagShift = 12;
 // emits its M-blocks' lists and the unit's merged step list.
 hipError_t launch_decode(const PlanTables& pt, const WorkTables& wt, const uint8_t* la,
                          const uint8_t* ca, int32_t* counts, int32_t* row_ptr, int32_t* col_idx,
-                         hipStream_t stream);
+                         const KvPages& pages, hipStream_t stream);
 
 // Merged step lists from caller-given per-M-block lists (entries outside
 // [first tile of the prompt, M-block] skipped; lists ascending).
@@ -75,6 +92,7 @@ struct AttnArgs {
   int32_t hq, hkv, head_dim, tile;
   float scale_log2;           // softmax scale * log2(e)
   int32_t out_f32;            // 1: fp32 output, 0: bf16 output
+  KvPages pages;              // K/V layout (table == nullptr: packed)
 };
 
 // bf16 attention reads the merged step lists of wt (not row_ptr/col_idx).

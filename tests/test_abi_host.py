@@ -14,7 +14,7 @@ def test_library_loads_and_exports_every_declared_symbol():
     L = B.lib()
     names = B.header_functions()
     assert "sift_sparse_prefill" in names and "sift_decode_tiles" in names
-    assert len(names) == 10
+    assert len(names) == 11
     for n in names:
         assert hasattr(L, n), n
     # the binding declares every one of them too
@@ -77,3 +77,4 @@ def test_plan_create_rejects_bad_layouts_on_the_host():
     assert B.lib().sift_plan_create(ctypes.byref(lay), 4, 2, 80, 64, ctypes.byref(h)) == 4
     assert B.lib().sift_plan_create(None, 4, 2, 128, 64, ctypes.byref(h)) == 1
     assert B.lib().sift_plan_destroy(None) == 0
+    assert B.lib().sift_plan_run_paged(None, None, None, None, None, None, None, 0.0, None, None) == 1
