@@ -103,7 +103,7 @@ typedef struct sift_plan_info {
   int32_t num_kv_heads;     /* Hkv                                          */
   int32_t head_dim;         /* D                                            */
   int32_t tile;             /* T                                            */
-  int32_t num_work_units;   /* attention work units (head, M-block pair)    */
+  int32_t num_work_units;   /* attention workgroups' units (pieces counted) */
   int64_t num_rows;         /* Hq * M; row_ptr holds num_rows + 1 entries   */
   int64_t list_capacity;    /* Hq * (dense causal tile count): >= any nnz   */
   int64_t la_bytes;         /* size local_bitmap must have                  */

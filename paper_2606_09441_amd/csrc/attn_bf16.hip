@@ -354,6 +354,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
                                                            AttnArgs a) {
   // K slot 0, K slot 1, V slot 0, V slot 1 (16 KB each)
   __shared__ __attribute__((aligned(1024))) __bf16 smem[4 * kTile];
+  // the unit's partial-result slot, parked in LDS for the epilogue so that
+  // no register is held across the main loop (every wavefront writes the
+  // same value and reads back its own write)
+  __shared__ int slot_park;
 
   const int unit = wt.sched[blockIdx.x];
   if (unit < 0) return;
@@ -372,6 +376,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
   const int row_bytes = kstride * 2;
   const int mine = wave < 2 ? m0 : m1;     // this wavefront's M-block (-1: none)
   const int qrow = (wave & 1) * 32 + l32;  // query row inside that M-block
+  slot_park = wt.unit_slot[unit];
   const float c = a.scale_log2;
   const __bf16* __restrict__ qp = static_cast<const __bf16*>(a.q);
   const __bf16* __restrict__ kp = static_cast<const __bf16*>(a.k);
@@ -534,11 +539,34 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
     }
   }
 
-  // ---- epilogue: O = O^T / l, lane writes dims 32db + 8i + 4hf .. +3 of its row
-  if (mine < 0 || qrow >= qlen) return;
+  // The lane index is taken afresh (mbcnt of an opaque zero) so that no
+  // per-lane index stays in a register across the main loop.
+  unsigned zero;
+  asm volatile("s_mov_b32 %0, 0" : "=s"(zero));
+  const int ln = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, zero));
+  const int row = (wave & 1) * 32 + (ln & 31);  // = qrow
+  const int half = ln >> 5;                     // = hf
+  if (mine < 0 || row >= qlen) return;
   const float lt = swap_sum(rs.lsum);
+
   const float inv = lt > 0.f ? 1.f / lt : 0.f;
-  const int64_t obase = (static_cast<int64_t>(qtok0 + qrow) * hq + h) * kD + 4 * hf;
+
+  // ---- lane writes O = O^T / l, dims 32db + 8i + 4hf .. +3 of its row, in
+  // the output's type.  A piece of a split unit writes to its slot instead
+  // (plus the row's reference max and sum, for the merge).  A unit's query
+  // rows are at most kUnitRows consecutive tokens (blocks m0, m0 + 1 are
+  // adjacent in the packed order), so token t goes to row t mod kUnitRows of
+  // the slot.  Both cases share one store sequence.
+  const int slot = __builtin_amdgcn_readfirstlane(slot_park);
+  const int tok = qtok0 + row;
+  void* obuf = a.out;
+  int64_t obase = (static_cast<int64_t>(tok) * hq + h) * kD + 4 * half;
+  if (slot >= 0) {
+    const int64_t slot_row = static_cast<int64_t>(slot) * kUnitRows + (tok & (kUnitRows - 1));
+    obuf = wt.part_o;
+    obase = slot_row * kD + 4 * half;
+    if (half == 0) wt.part_ml[slot_row] = make_float2(rs.mref, lt);
+  }
 #pragma unroll
   for (int db = 0; db < 4; ++db)
 #pragma unroll
@@ -547,16 +575,62 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
       f32x4 x = f32x4{rs.o[db][4 * i] * inv, rs.o[db][4 * i + 1] * inv,
                       rs.o[db][4 * i + 2] * inv, rs.o[db][4 * i + 3] * inv};
       if constexpr (kOutF32) {
-        *reinterpret_cast<f32x4*>(static_cast<float*>(a.out) + obase + d) = x;
+        *reinterpret_cast<f32x4*>(static_cast<float*>(obuf) + obase + d) = x;
       } else {
         const bf16x2 y0 = bf16x2{static_cast<__bf16>(x[0]), static_cast<__bf16>(x[1])};
         const bf16x2 y1 = bf16x2{static_cast<__bf16>(x[2]), static_cast<__bf16>(x[3])};
         u32x2 w;
         w[0] = __builtin_bit_cast(unsigned, y0);
         w[1] = __builtin_bit_cast(unsigned, y1);
-        *reinterpret_cast<u32x2*>(static_cast<__bf16*>(a.out) + obase + d) = w;
+        *reinterpret_cast<u32x2*>(static_cast<__bf16*>(obuf) + obase + d) = w;
       }
     }
+}
+
+// Merge the pieces of one split unit, one workgroup per unit.  Piece p
+// left its normalised output O_p (in the output's type), its reference max
+// m_p (log2 domain) and its row sum l_p, relative to 2^m_p.  With M the
+// largest m_p among pieces that saw keys and w_p = l_p 2^(m_p - M), the row's
+// output is sum w_p O_p / sum w_p.  Thread t owns row t/2 of the unit and
+// head-dim half t%2.
+template <bool kOutF32>
+__global__ __launch_bounds__(256) void combine_kernel(PlanTables pt, WorkTables wt, AttnArgs a) {
+  using OutT = typename std::conditional<kOutF32, float, __bf16>::type;
+  const int4 sp = wt.splits[blockIdx.x];  // {first work unit, first slot, slots}
+  const int w0 = sp.x;
+  const int h = wt.unit_head[w0];
+  const int row = threadIdx.x >> 1;
+  const int d0 = (threadIdx.x & 1) * (kD / 2);
+  const int blk = row >> 6;
+  const int r = row & 63;
+  if (blk >= wt.unit_nb[w0]) return;
+  const int m = wt.unit_m0[w0] + blk;
+  if (r >= pt.tile_len[m]) return;
+  const int tok = pt.tile_tok0[m] + r;
+  const int prow = tok & (kUnitRows - 1);  // the row's place in a slot
+  float mx = -INFINITY;
+  for (int p = 0; p < sp.z; ++p) {
+    const float2 ml = wt.part_ml[static_cast<int64_t>(sp.y + p) * kUnitRows + prow];
+    if (ml.y > 0.f) mx = fmaxf(mx, ml.x);
+  }
+  float acc[kD / 2];
+#pragma unroll
+  for (int j = 0; j < kD / 2; ++j) acc[j] = 0.f;
+  float wsum = 0.f;
+  for (int p = 0; p < sp.z; ++p) {
+    const int64_t slot_row = static_cast<int64_t>(sp.y + p) * kUnitRows + prow;
+    const float2 ml = wt.part_ml[slot_row];
+    if (!(ml.y > 0.f)) continue;
+    const float w = ml.y * __builtin_amdgcn_exp2f(ml.x - mx);
+    wsum += w;
+    const OutT* po = static_cast<const OutT*>(wt.part_o) + slot_row * kD + d0;
+#pragma unroll
+    for (int j = 0; j < kD / 2; ++j) acc[j] += w * static_cast<float>(po[j]);
+  }
+  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+  OutT* dst = static_cast<OutT*>(a.out) + (static_cast<int64_t>(tok) * a.hq + h) * kD + d0;
+#pragma unroll
+  for (int j = 0; j < kD / 2; ++j) dst[j] = static_cast<OutT>(acc[j] * inv);
 }
 
 }  // namespace
@@ -569,6 +643,13 @@ hipError_t launch_attn_bf16(const PlanTables& pt, const WorkTables& wt, const At
     hipLaunchKernelGGL(attn_bf16_kernel<true>, dim3(wt.grid), dim3(256), 0, stream, pt, wt, a);
   else
     hipLaunchKernelGGL(attn_bf16_kernel<false>, dim3(wt.grid), dim3(256), 0, stream, pt, wt, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || wt.num_splits == 0) return e;
+  if (a.out_f32)
+    hipLaunchKernelGGL(combine_kernel<true>, dim3(wt.num_splits), dim3(256), 0, stream, pt, wt, a);
+  else
+    hipLaunchKernelGGL(combine_kernel<false>, dim3(wt.num_splits), dim3(256), 0, stream, pt, wt,
+                       a);
   return hipGetLastError();
 }
 

@@ -167,9 +167,9 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   const int lane = threadIdx.x & 63;
   const int u = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (u >= wt.num_units) return;  // uniform per wavefront
-  const int h = wt.unit_head[u];
-  const int m0 = wt.unit_m0[u];
-  const int nb = wt.unit_nb[u];
+  const int h = wt.lu_head[u];
+  const int m0 = wt.lu_m0[u];
+  const int nb = wt.lu_nb[u];
   const unsigned all = (1u << nb) - 1u;
   const int64_t r0 = static_cast<int64_t>(h) * pt.num_tiles + m0;
   Emitter e;
@@ -179,7 +179,7 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   e.pages = pages;
 #pragma unroll
   for (int k = 0; k < kUnitBlocks; ++k) e.pos[k] = k < nb ? row_ptr[r0 + k] : 0;
-  e.ps = wt.step_off[u];
+  e.ps = wt.lu_off[u];
   e.m0 = m0;
   e.nb = nb;
   e.below = (1ull << lane) - 1ull;
@@ -222,7 +222,7 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
       e.emit(listed, pt.seg_tile0[s] + j);
     }
   }
-  if (lane == 0) wt.step_cnt[u] = e.ps - wt.step_off[u];
+  if (lane == 0) write_work_counts(wt, u, e.ps - wt.lu_off[u]);
 }
 
 // Generic merge of caller-given lists (one thread per unit): the union of
@@ -234,9 +234,9 @@ __global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
                                                    int64_t cap) {
   const int u = blockIdx.x * blockDim.x + threadIdx.x;
   if (u >= wt.num_units) return;
-  const int h = wt.unit_head[u];
-  const int m0 = wt.unit_m0[u];
-  const int nb = wt.unit_nb[u];
+  const int h = wt.lu_head[u];
+  const int m0 = wt.lu_m0[u];
+  const int nb = wt.lu_nb[u];
   const int lo = pt.tile_lo[m0];
   const int64_t r0 = static_cast<int64_t>(h) * pt.num_tiles + m0;
   auto clampi = [cap](int64_t x) { return min(cap, max(static_cast<int64_t>(0), x)); };
@@ -250,8 +250,8 @@ __global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
       end[k] = max(it[k], clampi(row_ptr[r0 + k + 1]));
     }
   }
-  const int base = wt.step_off[u];
-  const int room = wt.step_off[u + 1] - base;
+  const int base = wt.lu_off[u];
+  const int room = wt.lu_off[u + 1] - base;
   int ns = 0;
   while (ns < room) {
     int head[kUnitBlocks];
@@ -283,7 +283,7 @@ __global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
     wt.steps[base + ns] = make_int2(pt.tile_tok0[n], info);
     ++ns;
   }
-  wt.step_cnt[u] = ns;
+  write_work_counts(wt, u, ns);
 }
 
 }  // namespace

@@ -81,7 +81,11 @@ sift_status check_io(const sift_tensor* q, const sift_tensor* k, const sift_tens
 struct HostPlan {
   std::vector<int32_t> seg_tile0, seg_pages, seg_kind, seg_first, seg_la_off, seg_ca_off;
   std::vector<int32_t> tile_seg, tile_tok0, tile_len, tile_lo;
-  std::vector<int32_t> unit_head, unit_m0, unit_nb, sched, step_off;
+  std::vector<int32_t> unit_head, unit_m0, unit_nb, sched, step_off;  // list units
+  std::vector<int32_t> lu_work0, lu_nwork, lu_len;
+  std::vector<int32_t> wk_head, wk_m0, wk_nb, wk_off, wk_slot;        // work units
+  std::vector<int32_t> splits;  // int4 records (see WorkTables)
+  int64_t part_slots = 0;
   int64_t dense_tiles = 0;  // causal tiles of all prompts, one head
   int64_t la_bytes = 0, ca_bytes = 0;
   int32_t num_tokens = 0, num_segments = 0, num_tiles = 0;
@@ -209,15 +213,60 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
     if (hp.step_off[k] + unit_cost[k] > i32max) return SIFT_E_CAPACITY;
     hp.step_off[k + 1] = hp.step_off[k] + static_cast<int32_t>(unit_cost[k]);
   }
+  // Work units.  A query unit lists every tile of its prompt up to its last
+  // M-block, so its list length is its cost; it is cut into pieces of at
+  // most `piece` steps so that no workgroup walks a list much longer than a
+  // document unit's.  The piece length doubles until at most kMaxSlots
+  // partial slots are needed.
+  constexpr int64_t kMaxSlots = 4096;
+  auto is_query = [&](int64_t k) { return hp.seg_kind[hp.tile_seg[hp.unit_m0[k]]] == sift::kQuery; };
+  int64_t piece = 32;
+  auto slots_for = [&](int64_t pc) {
+    int64_t n = 0;
+    for (int64_t k = 0; k < U; ++k)
+      if (is_query(k) && unit_cost[k] > pc) n += (unit_cost[k] + pc - 1) / pc;
+    return n;
+  };
+  while (slots_for(piece) > kMaxSlots) piece *= 2;
+  hp.lu_work0.assign(U, 0);
+  hp.lu_nwork.assign(U, 1);
+  hp.lu_len.assign(U, 0);
+  std::vector<int64_t> wk_cost;
+  std::vector<int32_t> wk_order;  // work units in list-unit locality order
+  for (int32_t uu : order) {
+    const int64_t cost = unit_cost[uu];
+    const int64_t parts = is_query(uu) && cost > piece ? (cost + piece - 1) / piece : 1;
+    const int64_t len = (cost + parts - 1) / parts;
+    hp.lu_work0[uu] = static_cast<int32_t>(hp.wk_head.size());
+    hp.lu_nwork[uu] = static_cast<int32_t>(parts);
+    hp.lu_len[uu] = static_cast<int32_t>(len);
+    if (parts > 1)
+      hp.splits.insert(hp.splits.end(), {static_cast<int32_t>(hp.wk_head.size()),
+                                         static_cast<int32_t>(hp.part_slots),
+                                         static_cast<int32_t>(parts), 0});
+    for (int64_t i = 0; i < parts; ++i) {
+      wk_order.push_back(static_cast<int32_t>(hp.wk_head.size()));
+      hp.wk_head.push_back(hp.unit_head[uu]);
+      hp.wk_m0.push_back(hp.unit_m0[uu]);
+      hp.wk_nb.push_back(hp.unit_nb[uu]);
+      hp.wk_off.push_back(static_cast<int32_t>(hp.step_off[uu] + i * len));
+      hp.wk_slot.push_back(parts > 1 ? static_cast<int32_t>(hp.part_slots + i) : -1);
+      wk_cost.push_back(std::min(len, cost - i * len));
+    }
+    if (parts > 1) hp.part_slots += parts;
+  }
+  const int64_t W = static_cast<int64_t>(wk_cost.size());
+  if (W > i32max / 2) return SIFT_E_CAPACITY;
   // Split the locality order into kNumXcd contiguous chunks; workgroup
-  // x + kNumXcd * k runs chunk x's k-th unit (longest first inside a chunk).
+  // x + kNumXcd * k runs chunk x's k-th work unit (longest first inside a
+  // chunk).
   std::vector<std::vector<int32_t>> chunk(kNumXcd);
   int64_t longest = 0;
   for (int x = 0; x < kNumXcd; ++x) {
-    const int64_t a = U * x / kNumXcd, z = U * (x + 1) / kNumXcd;
-    chunk[x].assign(order.begin() + a, order.begin() + z);
+    const int64_t a = W * x / kNumXcd, z = W * (x + 1) / kNumXcd;
+    chunk[x].assign(wk_order.begin() + a, wk_order.begin() + z);
     std::stable_sort(chunk[x].begin(), chunk[x].end(),
-                     [&](int32_t p, int32_t q) { return unit_cost[p] > unit_cost[q]; });
+                     [&](int32_t p, int32_t q) { return wk_cost[p] > wk_cost[q]; });
     longest = std::max<int64_t>(longest, static_cast<int64_t>(chunk[x].size()));
   }
   hp.sched.assign(longest * kNumXcd, -1);
@@ -280,6 +329,15 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   const size_t o_um0 = put(blob, hp.unit_m0);
   const size_t o_unb = put(blob, hp.unit_nb);
   const size_t o_soff = put(blob, hp.step_off);
+  const size_t o_lw0 = put(blob, hp.lu_work0);
+  const size_t o_lnw = put(blob, hp.lu_nwork);
+  const size_t o_llen = put(blob, hp.lu_len);
+  const size_t o_wh = put(blob, hp.wk_head);
+  const size_t o_wm0 = put(blob, hp.wk_m0);
+  const size_t o_wnb = put(blob, hp.wk_nb);
+  const size_t o_woff = put(blob, hp.wk_off);
+  const size_t o_wslot = put(blob, hp.wk_slot);
+  const size_t o_splits = put(blob, hp.splits);
   const int64_t rows = static_cast<int64_t>(hp.num_tiles) * num_q_heads;
   const int64_t cap = hp.dense_tiles * num_q_heads;
   const int64_t U = static_cast<int64_t>(hp.unit_head.size());
@@ -287,10 +345,14 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   const size_t o_counts = align(blob.size());
   const size_t o_rowptr = align(o_counts + rows * 4);
   const size_t o_col = align(o_rowptr + (rows + 1) * 4);
+  const int64_t W = static_cast<int64_t>(hp.wk_head.size());
   const size_t o_scnt = align(o_col + std::max<int64_t>(cap, 1) * 4);
-  const size_t o_steps = align(o_scnt + std::max<int64_t>(U, 1) * 4);
+  const size_t o_steps = align(o_scnt + std::max<int64_t>(W, 1) * 4);
   // steps: the units' lists, plus a few entries read (never used) past the end
-  const size_t total = o_steps + (std::max<int64_t>(cap, 1) + 8) * 8;
+  const size_t o_part_o = align(o_steps + (std::max<int64_t>(cap, 1) + 8) * 8);
+  const int64_t slot_rows = hp.part_slots * sift::kUnitRows;
+  const size_t o_part_ml = align(o_part_o + slot_rows * head_dim * 4);  // fp32 or bf16 output
+  const size_t total = o_part_ml + std::max<int64_t>(slot_rows, 1) * 8;
 
   sift_plan* plan = new (std::nothrow) sift_plan();
   if (plan == nullptr) return SIFT_E_HIP;
@@ -326,13 +388,26 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   plan->pt.num_tiles = hp.num_tiles;
   plan->pt.num_q_heads = num_q_heads;
   plan->wt.sched = P(o_sched);
-  plan->wt.unit_head = P(o_uh);
-  plan->wt.unit_m0 = P(o_um0);
-  plan->wt.unit_nb = P(o_unb);
-  plan->wt.step_off = P(o_soff);
+  plan->wt.unit_head = P(o_wh);
+  plan->wt.unit_m0 = P(o_wm0);
+  plan->wt.unit_nb = P(o_wnb);
+  plan->wt.step_off = P(o_woff);
   plan->wt.step_cnt = P(o_scnt);
+  plan->wt.unit_slot = P(o_wslot);
+  plan->wt.lu_head = P(o_uh);
+  plan->wt.lu_m0 = P(o_um0);
+  plan->wt.lu_nb = P(o_unb);
+  plan->wt.lu_off = P(o_soff);
+  plan->wt.lu_work0 = P(o_lw0);
+  plan->wt.lu_nwork = P(o_lnw);
+  plan->wt.lu_len = P(o_llen);
   plan->wt.steps = reinterpret_cast<int2*>(P(o_steps));
+  plan->wt.splits = reinterpret_cast<const int4*>(P(o_splits));
+  plan->wt.part_o = static_cast<void*>(P(o_part_o));
+  plan->wt.part_ml = reinterpret_cast<float2*>(P(o_part_ml));
   plan->wt.num_units = static_cast<int32_t>(U);
+  plan->wt.num_work = static_cast<int32_t>(W);
+  plan->wt.num_splits = static_cast<int32_t>(hp.splits.size() / 4);
   plan->wt.grid = static_cast<int32_t>(hp.sched.size());
   plan->counts = P(o_counts);
   plan->row_ptr = P(o_rowptr);
@@ -346,7 +421,7 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   in.num_kv_heads = num_kv_heads;
   in.head_dim = head_dim;
   in.tile = tile;
-  in.num_work_units = static_cast<int32_t>(hp.unit_head.size());
+  in.num_work_units = static_cast<int32_t>(W);
   in.num_rows = rows;
   in.list_capacity = cap;
   in.la_bytes = hp.la_bytes;

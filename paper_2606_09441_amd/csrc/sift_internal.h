@@ -44,27 +44,61 @@ __device__ __forceinline__ int32_t kv_row0(const PlanTables& pt, const KvPages& 
   return (p < 0 ? 0 : (p >= pg.num_pages ? pg.num_pages - 1 : p)) * pt.tile;
 }
 
-// Attention work: one unit = (query head, up to kUnitBlocks consecutive
-// M-blocks of one segment).  sched[g] is the unit run by workgroup g, or -1
-// for none.  A unit's merged step list (the union of its M-blocks' lists, in
-// ascending key-tile order) lives at steps[step_off[u] .. step_off[u] +
-// step_cnt[u]); step_off[u+1] - step_off[u] bounds its length.
+// Attention work: a list unit = (query head, up to kUnitBlocks consecutive
+// M-blocks of one segment).  The decode pass writes each list unit's merged
+// step list (the union of its M-blocks' lists, in ascending key-tile order)
+// at steps[lu_off[u] ..]; lu_off[u+1] - lu_off[u] bounds its length.
 // Step = {first K/V row of the key tile, len | listed << 8 | diagonal << 12},
 // where bit k of `listed` says M-block m0 + k lists the tile and bit k of
 // `diagonal` says the tile is m0 + k itself.
+//
+// A workgroup runs one work unit: a list unit's whole step list, or one piece
+// of it.  The query units, whose lists are long and of known length, are cut
+// into pieces of at most a few dozen steps; a piece writes its partial result
+// (O normalised by its own row sum, in the output's type; reference max; row
+// sum) to a slot of the partial scratch, and a combine pass merges the pieces
+// of every split unit into the output.
+// List unit u owns work units lu_work0[u] .. + lu_nwork[u] - 1, piece k
+// covering its steps [k * lu_len[u], (k + 1) * lu_len[u]); decode writes
+// their step counts.
 constexpr int kUnitBlocks = 2;
+constexpr int kUnitRows = 64 * kUnitBlocks;  // query rows of a unit
 
 struct WorkTables {
-  const int32_t* sched;       // [grid]
-  const int32_t* unit_head;   // [U]
-  const int32_t* unit_m0;     // [U] first M-block
-  const int32_t* unit_nb;     // [U] M-blocks in the unit, 1 .. kUnitBlocks
-  const int32_t* step_off;    // [U + 1]
-  int32_t* step_cnt;          // [U] (device scratch)
-  int2* steps;                // [step_off[U]] (device scratch)
+  // work units (attention)
+  const int32_t* sched;       // [grid] work unit of each workgroup, or -1
+  const int32_t* unit_head;   // [W]
+  const int32_t* unit_m0;     // [W] first M-block
+  const int32_t* unit_nb;     // [W] M-blocks, 1 .. kUnitBlocks
+  const int32_t* step_off;    // [W] first step in steps
+  int32_t* step_cnt;          // [W] steps (device scratch, written by decode)
+  const int32_t* unit_slot;   // [W] partial slot, or -1: write the output
+  // list units (decode)
+  const int32_t* lu_head;     // [U]
+  const int32_t* lu_m0;       // [U]
+  const int32_t* lu_nb;       // [U]
+  const int32_t* lu_off;      // [U + 1]
+  const int32_t* lu_work0;    // [U]
+  const int32_t* lu_nwork;    // [U]
+  const int32_t* lu_len;      // [U] piece length (a bound of the list when not split)
+  int2* steps;                // [lu_off[U]] (device scratch)
+  const int4* splits;         // [NS] {first work unit, first slot, slots, 0}
+  void* part_o;               // [slots][kUnitRows][head_dim], output type (device scratch)
+  float2* part_ml;            // [slots][kUnitRows] {reference max, row sum}
   int32_t num_units;          // U
+  int32_t num_work;           // W
+  int32_t num_splits;         // NS
   int32_t grid;
 };
+
+// Step counts of a list unit's work units, from the length of its list.
+__device__ __forceinline__ void write_work_counts(const WorkTables& wt, int32_t u, int32_t cnt) {
+  const int32_t w0 = wt.lu_work0[u], nw = wt.lu_nwork[u], len = wt.lu_len[u];
+  for (int32_t k = 0; k < nw; ++k) {
+    const int32_t rest = cnt - k * len;
+    wt.step_cnt[w0 + k] = rest < 0 ? 0 : (rest > len ? len : rest);
+  }
+}
 
 constexpr int kStepLenMask = 0xff;
 constexpr int kStepListedShift = 8;
