@@ -359,11 +359,14 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
   // same value and reads back its own write)
   __shared__ int slot_park;
 
-  const int unit = wt.sched[blockIdx.x];
-  if (unit < 0) return;
-  const int h = wt.unit_head[unit];
-  const int m0 = wt.unit_m0[unit];
-  const int m1 = wt.unit_nb[unit] > 1 ? m0 + 1 : -1;
+  // the work unit's record, loaded whole before anything else
+  const int4* __restrict__ rp = reinterpret_cast<const int4*>(wt.launch + blockIdx.x);
+  const int4 ra = rp[0];  // head, kv head, blocks, slot
+  const int4 rb = rp[1];  // first token and length of the two M-blocks
+  const int4 rc = rp[2];  // step offset, step count, step 0
+  const int4 rd = rp[3];  // steps 1, 2
+  const int h = ra.x;
+  const int kvh = ra.y;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
@@ -371,12 +374,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
   const int hf = lane >> 5;
   const int hq = a.hq;
   const int hkv = a.hkv;
-  const int kvh = h / (hq / hkv);
   const int kstride = hkv * kD;
   const int row_bytes = kstride * 2;
-  const int mine = wave < 2 ? m0 : m1;     // this wavefront's M-block (-1: none)
-  const int qrow = (wave & 1) * 32 + l32;  // query row inside that M-block
-  slot_park = wt.unit_slot[unit];
+  const int qrow = (wave & 1) * 32 + l32;  // query row inside this wavefront's M-block
+  slot_park = ra.w;
   const float c = a.scale_log2;
   const __bf16* __restrict__ qp = static_cast<const __bf16*>(a.q);
   const __bf16* __restrict__ kp = static_cast<const __bf16*>(a.k);
@@ -403,11 +404,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
 
   // Q^T fragments (B operand of S^T = K Q^T): lane holds query row qrow,
   // dims 16s + 8hf .. +7 for k-step s.
-  int qtok0 = 0, qlen = 0;
-  if (mine >= 0) {
-    qtok0 = pt.tile_tok0[mine];
-    qlen = pt.tile_len[mine];
-  }
+  // wavefronts 0, 1 take M-block m0, wavefronts 2, 3 M-block m0 + 1 (a
+  // missing block has no rows)
+  const int qtok0 = wave < 2 ? rb.x : rb.y;
+  const int qlen = wave < 2 ? rb.z : rb.w;
   bf16x8 qf[8];
   {
     const bool live = qrow < qlen;
@@ -421,8 +421,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
   }
 
   // the unit's merged steps
-  const int2* __restrict__ steps = wt.steps + wt.step_off[unit];
-  const int nsteps = wt.step_cnt[unit];
+  const int2* __restrict__ steps = wt.steps + rc.x;
+  const int nsteps = rc.y;
   const int64_t kv_head_off = static_cast<int64_t>(kvh) * kD;
   auto rsrc = [&](const __bf16* base, const Step& s) {
     return tile_rsrc(base + static_cast<int64_t>(s.tok0) * kstride + kv_head_off, s.len(),
@@ -452,9 +452,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
   // an empty list leaves O = 0 and l = 0: the epilogue writes zeros
   if (nsteps > 0) {
     // ---- prologue: K(0), V(0), K(1) into LDS; S(0) = K(0) Q^T
-    Step c0 = make_step(fetch(0), true);
-    Step c1 = make_step(fetch(1), nsteps > 1);
-    Step c2 = make_step(fetch(2), nsteps > 2);
+    Step c0 = make_step(make_int2(rc.z, rc.w), true);
+    // steps past the count carry stale values: make_step marks them invalid
+    Step c1 = make_step(make_int2(rd.x, rd.y), nsteps > 1);
+    Step c2 = make_step(make_int2(rd.z, rd.w), nsteps > 2);
     dma_tile<true>(kdst[0], koff0, rstep, rsrc(kp, c0));
     dma_tile<false>(vdst[0], voff0, rstep, rsrc(vp, c0));
     dma_tile<true>(kdst[1], koff0, rstep, rsrc(kp, c1.valid ? c1 : c0));
@@ -546,7 +547,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
   const int ln = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, zero));
   const int row = (wave & 1) * 32 + (ln & 31);  // = qrow
   const int half = ln >> 5;                     // = hf
-  if (mine < 0 || row >= qlen) return;
+  if (row >= qlen) return;
   const float lt = swap_sum(rs.lsum);
 
   const float inv = lt > 0.f ? 1.f / lt : 0.f;
@@ -596,17 +597,15 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
 template <bool kOutF32>
 __global__ __launch_bounds__(256) void combine_kernel(PlanTables pt, WorkTables wt, AttnArgs a) {
   using OutT = typename std::conditional<kOutF32, float, __bf16>::type;
-  const int4 sp = wt.splits[blockIdx.x];  // {first work unit, first slot, slots}
-  const int w0 = sp.x;
-  const int h = wt.unit_head[w0];
+  const int4 sp = wt.splits[blockIdx.x];  // {record of the first piece, first slot, slots}
+  const WorkRec* __restrict__ rp = wt.rec + sp.x;
+  const int h = rp->head;
   const int row = threadIdx.x >> 1;
   const int d0 = (threadIdx.x & 1) * (kD / 2);
   const int blk = row >> 6;
   const int r = row & 63;
-  if (blk >= wt.unit_nb[w0]) return;
-  const int m = wt.unit_m0[w0] + blk;
-  if (r >= pt.tile_len[m]) return;
-  const int tok = pt.tile_tok0[m] + r;
+  if (r >= (blk == 0 ? rp->len[0] : rp->len[1])) return;
+  const int tok = (blk == 0 ? rp->tok0[0] : rp->tok0[1]) + r;
   const int prow = tok & (kUnitRows - 1);  // the row's place in a slot
   float mx = -INFINITY;
   for (int p = 0; p < sp.z; ++p) {

@@ -133,6 +133,9 @@ struct Emitter {
   int32_t* col;
   int2* steps;
   const PlanTables* pt;
+  const WorkTables* wt;
+  int32_t u;     // list unit
+  int32_t base;  // its first step
   KvPages pages;
   int32_t pos[kUnitBlocks];  // next write position in each M-block's list
   int32_t ps;                // next write position in the step list
@@ -153,7 +156,10 @@ struct Emitter {
       const unsigned diag = (n >= m0 && n < m0 + nb) ? 1u << (n - m0) : 0u;
       const int info = pt->tile_len[n] | static_cast<int>(listed << kStepListedShift) |
                        static_cast<int>(diag << kStepDiagShift);
-      steps[ps + __popcll(mu & below)] = make_int2(kv_row0(*pt, pages, n), info);
+      const int32_t idx = ps + __popcll(mu & below);
+      const int2 st = make_int2(kv_row0(*pt, pages, n), info);
+      steps[idx] = st;
+      note_step(*wt, u, idx - base, st);
     }
     ps += __popcll(mu);
   }
@@ -180,6 +186,9 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
 #pragma unroll
   for (int k = 0; k < kUnitBlocks; ++k) e.pos[k] = k < nb ? row_ptr[r0 + k] : 0;
   e.ps = wt.lu_off[u];
+  e.wt = &wt;
+  e.u = u;
+  e.base = e.ps;
   e.m0 = m0;
   e.nb = nb;
   e.below = (1ull << lane) - 1ull;
@@ -227,7 +236,7 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
 
 // Generic merge of caller-given lists (one thread per unit): the union of
 // the unit's rows, ascending, entries outside [first tile of the prompt,
-// M-block] skipped, at most step_off[u+1] - step_off[u] steps.
+// M-block] skipped, at most lu_off[u+1] - lu_off[u] steps.
 __global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
                                                    const int32_t* __restrict__ row_ptr,
                                                    const int32_t* __restrict__ col,
@@ -280,10 +289,75 @@ __global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
     const unsigned diag = (n >= m0 && n < m0 + nb) ? 1u << (n - m0) : 0u;
     const int info = pt.tile_len[n] | static_cast<int>(listed << kStepListedShift) |
                      static_cast<int>(diag << kStepDiagShift);
-    wt.steps[base + ns] = make_int2(pt.tile_tok0[n], info);
+    const int2 st = make_int2(pt.tile_tok0[n], info);
+    wt.steps[base + ns] = st;
+    note_step(wt, u, ns, st);
     ++ns;
   }
   write_work_counts(wt, u, ns);
+}
+
+// Schedule pass: block (x, j) places work units j * 256 .. of chunk x at
+// launch[x + kNumXcd * (bucket offset + rank)], after scanning the chunk's
+// kSchedBuckets bucket sizes (4 per thread); the last block to finish
+// clears the buckets.
+__global__ __launch_bounds__(256) void schedule_scatter(WorkTables wt) {
+  __shared__ int32_t off[kSchedBuckets];
+  __shared__ int32_t wsum[4];
+  __shared__ int32_t last;
+  const int t = threadIdx.x;
+  const int lane = t & 63;
+  const int wave = t >> 6;
+  const int x = blockIdx.y;
+  const int32_t* hist = wt.hist + x * kSchedBuckets;
+  int32_t v[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) v[k] = hist[4 * t + k];
+  const int32_t own = v[0] + v[1] + v[2] + v[3];
+  int32_t s = own;  // inclusive scan of the thread sums inside the wavefront
+  for (int o = 1; o < 64; o <<= 1) {
+    const int32_t y = __shfl_up(s, o, 64);
+    if (lane >= o) s += y;
+  }
+  if (lane == 63) wsum[wave] = s;
+  __syncthreads();
+  int32_t e = s - own;
+  for (int j = 0; j < wave; ++j) e += wsum[j];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    off[4 * t + k] = e;
+    e += v[k];
+  }
+  __syncthreads();
+  const int32_t i = blockIdx.x * 256 + t;  // place in the chunk
+  const int32_t w = x * wt.chunk_size + i;
+  if (i < wt.chunk_size && w < wt.num_work) {
+    const int32_t k = off[sched_bucket(wt.rec[w].step_cnt)] + wt.rank[w];
+    if (k >= 0 && k < wt.chunk_size) {
+      const int4* src = reinterpret_cast<const int4*>(wt.rec + w);
+      int4* dst = reinterpret_cast<int4*>(wt.launch + x + kNumXcd * k);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) dst[q] = src[q];
+    }
+  }
+  __syncthreads();  // this block's reads of hist are done
+  if (t == 0) {
+    __threadfence();
+    const int32_t nblk = static_cast<int32_t>(gridDim.x * gridDim.y);
+    last = atomicAdd(&wt.hist[kNumXcd * kSchedBuckets], 1) == nblk - 1;
+  }
+  __syncthreads();
+  if (last) {
+    for (int q = t; q <= kNumXcd * kSchedBuckets; q += 256) wt.hist[q] = 0;
+  }
+}
+
+hipError_t launch_schedule(const WorkTables& wt, hipStream_t stream) {
+  if (wt.num_work == 0) return hipSuccess;
+  hipLaunchKernelGGL(schedule_scatter,
+                     dim3(static_cast<unsigned>((wt.chunk_size + 255) / 256), kNumXcd), dim3(256),
+                     0, stream, wt);
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -306,7 +380,9 @@ hipError_t launch_decode(const PlanTables& pt, const WorkTables& wt, const uint8
   if (wt.num_units == 0) return hipSuccess;
   hipLaunchKernelGGL(decode_write, dim3(static_cast<unsigned>((wt.num_units + 3) / 4)), dim3(256),
                      0, stream, pt, wt, la, ca, row_ptr, col_idx, pages);
-  return hipGetLastError();
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_schedule(wt, stream);
 }
 
 hipError_t launch_merge_steps(const PlanTables& pt, const WorkTables& wt, const int32_t* row_ptr,
@@ -314,7 +390,9 @@ hipError_t launch_merge_steps(const PlanTables& pt, const WorkTables& wt, const 
   if (wt.num_units == 0) return hipSuccess;
   hipLaunchKernelGGL(merge_steps, dim3(static_cast<unsigned>((wt.num_units + 255) / 256)),
                      dim3(256), 0, stream, pt, wt, row_ptr, col_idx, col_capacity);
-  return hipGetLastError();
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_schedule(wt, stream);
 }
 
 }  // namespace sift

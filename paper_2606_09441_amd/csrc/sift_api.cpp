@@ -18,7 +18,6 @@
 
 namespace {
 
-constexpr int kNumXcd = 8;  // MI355X: workgroups are dealt round-robin over 8 XCDs
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 int64_t la_nbytes(int64_t P) { return ceil_div(P * (P + 1), 16); }  // Section 4.3
@@ -81,10 +80,13 @@ sift_status check_io(const sift_tensor* q, const sift_tensor* k, const sift_tens
 struct HostPlan {
   std::vector<int32_t> seg_tile0, seg_pages, seg_kind, seg_first, seg_la_off, seg_ca_off;
   std::vector<int32_t> tile_seg, tile_tok0, tile_len, tile_lo;
-  std::vector<int32_t> unit_head, unit_m0, unit_nb, sched, step_off;  // list units
+  std::vector<int32_t> unit_head, unit_m0, unit_nb, step_off;  // list units
   std::vector<int32_t> lu_work0, lu_nwork, lu_len;
   std::vector<int32_t> wk_head, wk_m0, wk_nb, wk_off, wk_slot;        // work units
   std::vector<int32_t> splits;  // int4 records (see WorkTables)
+  std::vector<sift::WorkRec> rec;     // work units in locality order
+  std::vector<sift::WorkRec> launch;  // launch slots, initially empty
+  int64_t chunk_size = 0;
   int64_t part_slots = 0;
   int64_t dense_tiles = 0;  // causal tiles of all prompts, one head
   int64_t la_bytes = 0, ca_bytes = 0;
@@ -231,8 +233,7 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
   hp.lu_work0.assign(U, 0);
   hp.lu_nwork.assign(U, 1);
   hp.lu_len.assign(U, 0);
-  std::vector<int64_t> wk_cost;
-  std::vector<int32_t> wk_order;  // work units in list-unit locality order
+  int64_t W = 0;
   for (int32_t uu : order) {
     const int64_t cost = unit_cost[uu];
     const int64_t parts = is_query(uu) && cost > piece ? (cost + piece - 1) / piece : 1;
@@ -245,33 +246,39 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
                                          static_cast<int32_t>(hp.part_slots),
                                          static_cast<int32_t>(parts), 0});
     for (int64_t i = 0; i < parts; ++i) {
-      wk_order.push_back(static_cast<int32_t>(hp.wk_head.size()));
+      ++W;
       hp.wk_head.push_back(hp.unit_head[uu]);
       hp.wk_m0.push_back(hp.unit_m0[uu]);
       hp.wk_nb.push_back(hp.unit_nb[uu]);
       hp.wk_off.push_back(static_cast<int32_t>(hp.step_off[uu] + i * len));
       hp.wk_slot.push_back(parts > 1 ? static_cast<int32_t>(hp.part_slots + i) : -1);
-      wk_cost.push_back(std::min(len, cost - i * len));
     }
     if (parts > 1) hp.part_slots += parts;
   }
-  const int64_t W = static_cast<int64_t>(wk_cost.size());
   if (W > i32max / 2) return SIFT_E_CAPACITY;
-  // Split the locality order into kNumXcd contiguous chunks; workgroup
-  // x + kNumXcd * k runs chunk x's k-th work unit (longest first inside a
-  // chunk).
-  std::vector<std::vector<int32_t>> chunk(kNumXcd);
-  int64_t longest = 0;
-  for (int x = 0; x < kNumXcd; ++x) {
-    const int64_t a = W * x / kNumXcd, z = W * (x + 1) / kNumXcd;
-    chunk[x].assign(wk_order.begin() + a, wk_order.begin() + z);
-    std::stable_sort(chunk[x].begin(), chunk[x].end(),
-                     [&](int32_t p, int32_t q) { return wk_cost[p] > wk_cost[q]; });
-    longest = std::max<int64_t>(longest, static_cast<int64_t>(chunk[x].size()));
+  // Work-unit records in locality order (work unit w is record w); the
+  // launch order is made on the device after each decode, from the step
+  // counts.
+  hp.rec.assign(W, sift::WorkRec{});
+  for (int64_t w = 0; w < W; ++w) {
+    sift::WorkRec& r = hp.rec[w];
+    r.head = hp.wk_head[w];
+    r.kv_head = hp.wk_head[w] / (hq / hkv);
+    r.nb = hp.wk_nb[w];
+    r.slot = hp.wk_slot[w];
+    for (int b = 0; b < r.nb; ++b) {
+      r.tok0[b] = hp.tile_tok0[hp.wk_m0[w] + b];
+      r.len[b] = hp.tile_len[hp.wk_m0[w] + b];
+    }
+    r.step_off = hp.wk_off[w];
   }
-  hp.sched.assign(longest * kNumXcd, -1);
-  for (int x = 0; x < kNumXcd; ++x)
-    for (size_t k = 0; k < chunk[x].size(); ++k) hp.sched[x + kNumXcd * k] = chunk[x][k];
+  // launch slots start empty (one M-block of no rows, no steps); the
+  // schedule pass fills those of the work units
+  hp.chunk_size = (W + sift::kNumXcd - 1) / sift::kNumXcd;
+  sift::WorkRec empty{};
+  empty.nb = 1;
+  empty.slot = -1;
+  hp.launch.assign(hp.chunk_size * sift::kNumXcd, empty);
   return SIFT_OK;
 }
 
@@ -324,7 +331,6 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   const size_t o_tile_tok0 = put(blob, hp.tile_tok0);
   const size_t o_tile_len = put(blob, hp.tile_len);
   const size_t o_tile_lo = put(blob, hp.tile_lo);
-  const size_t o_sched = put(blob, hp.sched);
   const size_t o_uh = put(blob, hp.unit_head);
   const size_t o_um0 = put(blob, hp.unit_m0);
   const size_t o_unb = put(blob, hp.unit_nb);
@@ -332,11 +338,8 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   const size_t o_lw0 = put(blob, hp.lu_work0);
   const size_t o_lnw = put(blob, hp.lu_nwork);
   const size_t o_llen = put(blob, hp.lu_len);
-  const size_t o_wh = put(blob, hp.wk_head);
-  const size_t o_wm0 = put(blob, hp.wk_m0);
-  const size_t o_wnb = put(blob, hp.wk_nb);
-  const size_t o_woff = put(blob, hp.wk_off);
-  const size_t o_wslot = put(blob, hp.wk_slot);
+  const size_t o_rec = put(blob, hp.rec);  // step counts and first steps: written by decode
+  const size_t o_launch = put(blob, hp.launch);  // written by the schedule pass
   const size_t o_splits = put(blob, hp.splits);
   const int64_t rows = static_cast<int64_t>(hp.num_tiles) * num_q_heads;
   const int64_t cap = hp.dense_tiles * num_q_heads;
@@ -346,10 +349,12 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   const size_t o_rowptr = align(o_counts + rows * 4);
   const size_t o_col = align(o_rowptr + (rows + 1) * 4);
   const int64_t W = static_cast<int64_t>(hp.wk_head.size());
-  const size_t o_scnt = align(o_col + std::max<int64_t>(cap, 1) * 4);
-  const size_t o_steps = align(o_scnt + std::max<int64_t>(W, 1) * 4);
+  const size_t o_steps = align(o_col + std::max<int64_t>(cap, 1) * 4);
   // steps: the units' lists, plus a few entries read (never used) past the end
-  const size_t o_part_o = align(o_steps + (std::max<int64_t>(cap, 1) + 8) * 8);
+  const size_t o_rank = align(o_steps + (std::max<int64_t>(cap, 1) + 8) * 8);
+  const size_t o_hist = align(o_rank + std::max<int64_t>(W, 1) * 4);
+  constexpr size_t kHistBytes = (sift::kNumXcd * sift::kSchedBuckets + 1) * 4;
+  const size_t o_part_o = align(o_hist + kHistBytes);
   const int64_t slot_rows = hp.part_slots * sift::kUnitRows;
   const size_t o_part_ml = align(o_part_o + slot_rows * head_dim * 4);  // fp32 or bf16 output
   const size_t total = o_part_ml + std::max<int64_t>(slot_rows, 1) * 8;
@@ -371,6 +376,13 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
     delete plan;
     return SIFT_E_HIP;
   }
+  // the schedule's bucket sizes start at zero; each schedule pass leaves them so
+  if (hipMemset(static_cast<uint8_t*>(plan->dev) + o_hist, 0, kHistBytes) !=
+      hipSuccess) {
+    (void)hipFree(plan->dev);
+    delete plan;
+    return SIFT_E_HIP;
+  }
   auto P = [plan](size_t off) {
     return reinterpret_cast<int32_t*>(static_cast<uint8_t*>(plan->dev) + off);
   };
@@ -387,13 +399,10 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   plan->pt.tile = tile;
   plan->pt.num_tiles = hp.num_tiles;
   plan->pt.num_q_heads = num_q_heads;
-  plan->wt.sched = P(o_sched);
-  plan->wt.unit_head = P(o_wh);
-  plan->wt.unit_m0 = P(o_wm0);
-  plan->wt.unit_nb = P(o_wnb);
-  plan->wt.step_off = P(o_woff);
-  plan->wt.step_cnt = P(o_scnt);
-  plan->wt.unit_slot = P(o_wslot);
+  plan->wt.rec = reinterpret_cast<sift::WorkRec*>(P(o_rec));
+  plan->wt.launch = reinterpret_cast<sift::WorkRec*>(P(o_launch));
+  plan->wt.rank = P(o_rank);
+  plan->wt.hist = P(o_hist);
   plan->wt.lu_head = P(o_uh);
   plan->wt.lu_m0 = P(o_um0);
   plan->wt.lu_nb = P(o_unb);
@@ -408,7 +417,8 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   plan->wt.num_units = static_cast<int32_t>(U);
   plan->wt.num_work = static_cast<int32_t>(W);
   plan->wt.num_splits = static_cast<int32_t>(hp.splits.size() / 4);
-  plan->wt.grid = static_cast<int32_t>(hp.sched.size());
+  plan->wt.chunk_size = static_cast<int32_t>(hp.chunk_size);
+  plan->wt.grid = static_cast<int32_t>(hp.launch.size());
   plan->counts = P(o_counts);
   plan->row_ptr = P(o_rowptr);
   plan->col_idx = P(o_col);

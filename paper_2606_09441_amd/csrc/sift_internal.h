@@ -59,20 +59,55 @@ __device__ __forceinline__ int32_t kv_row0(const PlanTables& pt, const KvPages& 
 // sum) to a slot of the partial scratch, and a combine pass merges the pieces
 // of every split unit into the output.
 // List unit u owns work units lu_work0[u] .. + lu_nwork[u] - 1, piece k
-// covering its steps [k * lu_len[u], (k + 1) * lu_len[u]); decode writes
-// their step counts.
+// covering its steps [k * lu_len[u], (k + 1) * lu_len[u]).
+//
+// Every work unit has a 64-byte record that holds all a workgroup needs
+// before its first K/V fetch, so the kernel's start is one scalar load deep.
+// rec[w] (work units in locality order) is the planner's static part plus
+// the step count and first kFirstSteps steps, written by decode.
+//
+// Launch order.  Workgroups are dealt round-robin over the kNumXcd XCDs, so
+// workgroup x + kNumXcd * k runs on XCD x.  The locality order is cut into
+// kNumXcd chunks of chunk_size work units (w / chunk_size), chunk x for XCD
+// x, so that the query heads sharing key tiles share an L2.  Inside a chunk
+// the work units run in order of decreasing step count: the long ones start
+// first and the short ones fill the end.  Decode ends with a schedule pass
+// that copies each record to launch[x + kNumXcd * k], k its place in that
+// order (launch slots past a chunk's end hold an empty record: one M-block
+// of no rows, no steps).  The order is a counting sort: decode takes each
+// work unit's rank in its (chunk, count) bucket with an atomic on hist[],
+// and the schedule pass scans hist and scatters (then clears hist).
+constexpr int kNumXcd = 8;  // MI355X
 constexpr int kUnitBlocks = 2;
 constexpr int kUnitRows = 64 * kUnitBlocks;  // query rows of a unit
+constexpr int kFirstSteps = 3;
+constexpr int kSchedBuckets = 1024;          // step counts >= 1023 share bucket 0
+
+// Bucket of a step count: decreasing counts in increasing bucket order.
+__device__ __forceinline__ int32_t sched_bucket(int32_t cnt) {
+  return cnt >= kSchedBuckets - 1 ? 0 : kSchedBuckets - 1 - cnt;
+}
+
+struct alignas(64) WorkRec {
+  int32_t head;      // query head
+  int32_t kv_head;   // its K/V head
+  int32_t nb;        // M-blocks, 1 .. kUnitBlocks
+  int32_t slot;      // partial slot, or -1: write the output
+  int32_t tok0[kUnitBlocks];  // first token of each M-block (0 when absent)
+  int32_t len[kUnitBlocks];   // tokens of each M-block (0 when absent)
+  int32_t step_off;  // first step in steps
+  int32_t step_cnt;  // steps (written by decode)
+  int2 first[kFirstSteps];    // steps 0 .. kFirstSteps - 1 (written by decode; those past
+                              // step_cnt are stale)
+};
+static_assert(sizeof(WorkRec) == 64, "one record per 64 bytes");
 
 struct WorkTables {
-  // work units (attention)
-  const int32_t* sched;       // [grid] work unit of each workgroup, or -1
-  const int32_t* unit_head;   // [W]
-  const int32_t* unit_m0;     // [W] first M-block
-  const int32_t* unit_nb;     // [W] M-blocks, 1 .. kUnitBlocks
-  const int32_t* step_off;    // [W] first step in steps
-  int32_t* step_cnt;          // [W] steps (device scratch, written by decode)
-  const int32_t* unit_slot;   // [W] partial slot, or -1: write the output
+  WorkRec* rec;               // [W] locality order (device memory)
+  WorkRec* launch;            // [grid] launch order (device scratch, written by the schedule pass)
+  int32_t* rank;              // [W] rank in its (chunk, count) bucket (device scratch)
+  int32_t* hist;              // [kNumXcd * kSchedBuckets + 1] bucket sizes, then a workgroup
+                              // counter (device scratch, zero between decodes)
   // list units (decode)
   const int32_t* lu_head;     // [U]
   const int32_t* lu_m0;       // [U]
@@ -82,21 +117,39 @@ struct WorkTables {
   const int32_t* lu_nwork;    // [U]
   const int32_t* lu_len;      // [U] piece length (a bound of the list when not split)
   int2* steps;                // [lu_off[U]] (device scratch)
-  const int4* splits;         // [NS] {first work unit, first slot, slots, 0}
+  const int4* splits;         // [NS] {record of the first piece, first slot, slots, 0}
   void* part_o;               // [slots][kUnitRows][head_dim], output type (device scratch)
   float2* part_ml;            // [slots][kUnitRows] {reference max, row sum}
   int32_t num_units;          // U
   int32_t num_work;           // W
   int32_t num_splits;         // NS
-  int32_t grid;
+  int32_t chunk_size;         // work units per XCD chunk
+  int32_t grid;               // kNumXcd * chunk_size
 };
 
-// Step counts of a list unit's work units, from the length of its list.
+// Step `rel` of list unit u's list, just written: copy it into the record of
+// the piece it opens when it is one of that piece's first kFirstSteps.
+__device__ __forceinline__ void note_step(const WorkTables& wt, int32_t u, int32_t rel, int2 st) {
+  const int32_t nw = wt.lu_nwork[u];
+  int32_t k = 0, j = rel;
+  if (nw > 1) {
+    const int32_t len = wt.lu_len[u];
+    k = rel / len;
+    j = rel - k * len;
+  }
+  if (j < kFirstSteps && k < nw) wt.rec[wt.lu_work0[u] + k].first[j] = st;
+}
+
+// Step counts of a list unit's work units, from the length of its list,
+// and their ranks in their count buckets.
 __device__ __forceinline__ void write_work_counts(const WorkTables& wt, int32_t u, int32_t cnt) {
   const int32_t w0 = wt.lu_work0[u], nw = wt.lu_nwork[u], len = wt.lu_len[u];
   for (int32_t k = 0; k < nw; ++k) {
     const int32_t rest = cnt - k * len;
-    wt.step_cnt[w0 + k] = rest < 0 ? 0 : (rest > len ? len : rest);
+    const int32_t c = rest < 0 ? 0 : (rest > len ? len : rest);
+    wt.rec[w0 + k].step_cnt = c;
+    const int32_t x = (w0 + k) / wt.chunk_size;
+    wt.rank[w0 + k] = atomicAdd(&wt.hist[x * kSchedBuckets + sched_bucket(c)], 1);
   }
 }
 
