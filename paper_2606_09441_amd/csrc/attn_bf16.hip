@@ -588,48 +588,79 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
     }
 }
 
-// Merge the pieces of one split unit, one workgroup per unit.  Piece p
-// left its normalised output O_p (in the output's type), its reference max
-// m_p (log2 domain) and its row sum l_p, relative to 2^m_p.  With M the
-// largest m_p among pieces that saw keys and w_p = l_p 2^(m_p - M), the row's
-// output is sum w_p O_p / sum w_p.  Thread t owns row t/2 of the unit and
-// head-dim half t%2.
+// Merge the pieces of the split units.  Piece p left its normalised
+// output O_p (in the output's type), its reference max m_p (log2 domain) and
+// its row sum l_p, relative to 2^m_p.  With M the largest m_p among pieces
+// that saw keys and w_p = l_p 2^(m_p - M), a row's output is
+// sum w_p O_p / sum w_p.  Block (s, y) takes rows 32y .. 32y + 31 of split
+// unit s; thread t owns row 32y + t/8 and head dims 16 (t%8) .. + 15.
 template <bool kOutF32>
 __global__ __launch_bounds__(256) void combine_kernel(PlanTables pt, WorkTables wt, AttnArgs a) {
   using OutT = typename std::conditional<kOutF32, float, __bf16>::type;
+  constexpr int kDims = 16;                         // per thread
+  constexpr int kVec = 16 / sizeof(OutT);           // elements per 16-byte load
   const int4 sp = wt.splits[blockIdx.x];  // {record of the first piece, first slot, slots}
   const WorkRec* __restrict__ rp = wt.rec + sp.x;
-  const int h = rp->head;
-  const int row = threadIdx.x >> 1;
-  const int d0 = (threadIdx.x & 1) * (kD / 2);
+  const int row = blockIdx.y * 32 + (threadIdx.x >> 3);
+  const int d0 = (threadIdx.x & 7) * kDims;
   const int blk = row >> 6;
   const int r = row & 63;
   if (r >= (blk == 0 ? rp->len[0] : rp->len[1])) return;
   const int tok = (blk == 0 ? rp->tok0[0] : rp->tok0[1]) + r;
   const int prow = tok & (kUnitRows - 1);  // the row's place in a slot
+  const float2* ml = wt.part_ml + static_cast<int64_t>(sp.y) * kUnitRows + prow;
   float mx = -INFINITY;
+#pragma unroll 4
   for (int p = 0; p < sp.z; ++p) {
-    const float2 ml = wt.part_ml[static_cast<int64_t>(sp.y + p) * kUnitRows + prow];
-    if (ml.y > 0.f) mx = fmaxf(mx, ml.x);
+    const float2 x = ml[static_cast<int64_t>(p) * kUnitRows];
+    if (x.y > 0.f) mx = fmaxf(mx, x.x);
   }
-  float acc[kD / 2];
+  float acc[kDims];
 #pragma unroll
-  for (int j = 0; j < kD / 2; ++j) acc[j] = 0.f;
+  for (int j = 0; j < kDims; ++j) acc[j] = 0.f;
   float wsum = 0.f;
+  const OutT* po = static_cast<const OutT*>(wt.part_o) +
+                   (static_cast<int64_t>(sp.y) * kUnitRows + prow) * kD + d0;
+#pragma unroll 2
   for (int p = 0; p < sp.z; ++p) {
-    const int64_t slot_row = static_cast<int64_t>(sp.y + p) * kUnitRows + prow;
-    const float2 ml = wt.part_ml[slot_row];
-    if (!(ml.y > 0.f)) continue;
-    const float w = ml.y * __builtin_amdgcn_exp2f(ml.x - mx);
+    const float2 x = ml[static_cast<int64_t>(p) * kUnitRows];
+    const float w = x.y > 0.f ? x.y * __builtin_amdgcn_exp2f(x.x - mx) : 0.f;
     wsum += w;
-    const OutT* po = static_cast<const OutT*>(wt.part_o) + slot_row * kD + d0;
+    const OutT* src = po + static_cast<int64_t>(p) * kUnitRows * kD;
 #pragma unroll
-    for (int j = 0; j < kD / 2; ++j) acc[j] += w * static_cast<float>(po[j]);
+    for (int c = 0; c < kDims / kVec; ++c) {
+      const u32x4 raw = *reinterpret_cast<const u32x4*>(src + c * kVec);
+      if constexpr (kOutF32) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[4 * c + e] += w * __builtin_bit_cast(float, raw[e]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {  // bf16 -> f32 is exact: the high half of the word
+          const unsigned u = raw[e];
+          acc[8 * c + 2 * e] += w * __builtin_bit_cast(float, u << 16);
+          acc[8 * c + 2 * e + 1] += w * __builtin_bit_cast(float, u & 0xffff0000u);
+        }
+      }
+    }
   }
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-  OutT* dst = static_cast<OutT*>(a.out) + (static_cast<int64_t>(tok) * a.hq + h) * kD + d0;
+  OutT* dst = static_cast<OutT*>(a.out) + (static_cast<int64_t>(tok) * a.hq + rp->head) * kD + d0;
 #pragma unroll
-  for (int j = 0; j < kD / 2; ++j) dst[j] = static_cast<OutT>(acc[j] * inv);
+  for (int c = 0; c < kDims / kVec; ++c) {
+    u32x4 raw;
+    if constexpr (kOutF32) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) raw[e] = __builtin_bit_cast(unsigned, acc[4 * c + e] * inv);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bf16x2 y = bf16x2{static_cast<__bf16>(acc[8 * c + 2 * e] * inv),
+                                static_cast<__bf16>(acc[8 * c + 2 * e + 1] * inv)};
+        raw[e] = __builtin_bit_cast(unsigned, y);
+      }
+    }
+    *reinterpret_cast<u32x4*>(dst + c * kVec) = raw;
+  }
 }
 
 }  // namespace
@@ -645,10 +676,11 @@ hipError_t launch_attn_bf16(const PlanTables& pt, const WorkTables& wt, const At
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || wt.num_splits == 0) return e;
   if (a.out_f32)
-    hipLaunchKernelGGL(combine_kernel<true>, dim3(wt.num_splits), dim3(256), 0, stream, pt, wt, a);
+    hipLaunchKernelGGL(combine_kernel<true>, dim3(wt.num_splits, kUnitRows / 32), dim3(256), 0,
+                       stream, pt, wt, a);
   else
-    hipLaunchKernelGGL(combine_kernel<false>, dim3(wt.num_splits), dim3(256), 0, stream, pt, wt,
-                       a);
+    hipLaunchKernelGGL(combine_kernel<false>, dim3(wt.num_splits, kUnitRows / 32), dim3(256), 0,
+                       stream, pt, wt, a);
   return hipGetLastError();
 }
 

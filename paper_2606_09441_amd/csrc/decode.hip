@@ -134,8 +134,9 @@ struct Emitter {
   int2* steps;
   const PlanTables* pt;
   const WorkTables* wt;
-  int32_t u;     // list unit
-  int32_t base;  // its first step
+  int32_t base;  // the list unit's first step
+  int32_t w0;    // its first work unit
+  bool whole;    // not split: the first steps go to w0's record here
   KvPages pages;
   int32_t pos[kUnitBlocks];  // next write position in each M-block's list
   int32_t ps;                // next write position in the step list
@@ -159,7 +160,7 @@ struct Emitter {
       const int32_t idx = ps + __popcll(mu & below);
       const int2 st = make_int2(kv_row0(*pt, pages, n), info);
       steps[idx] = st;
-      note_step(*wt, u, idx - base, st);
+      if (whole && idx - base < kFirstSteps) wt->rec[w0].first[idx - base] = st;
     }
     ps += __popcll(mu);
   }
@@ -187,8 +188,9 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   for (int k = 0; k < kUnitBlocks; ++k) e.pos[k] = k < nb ? row_ptr[r0 + k] : 0;
   e.ps = wt.lu_off[u];
   e.wt = &wt;
-  e.u = u;
   e.base = e.ps;
+  e.w0 = wt.lu_work0[u];
+  e.whole = wt.lu_nwork[u] == 1;
   e.m0 = m0;
   e.nb = nb;
   e.below = (1ull << lane) - 1ull;
@@ -231,7 +233,18 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
       e.emit(listed, pt.seg_tile0[s] + j);
     }
   }
-  if (lane == 0) write_work_counts(wt, u, e.ps - wt.lu_off[u]);
+  const int32_t cnt = e.ps - e.base;
+  if (!e.whole) {
+    // the first steps of every piece, read back from the finished list
+    // (the fence makes this wavefront's stores visible to its loads)
+    __threadfence();
+    const int32_t nw = wt.lu_nwork[u], len = wt.lu_len[u];
+    for (int q = lane; q < nw * kFirstSteps; q += 64) {
+      const int32_t k = q / kFirstSteps, j = q - k * kFirstSteps;
+      if (k * len + j < cnt) wt.rec[e.w0 + k].first[j] = wt.steps[e.base + k * len + j];
+    }
+  }
+  if (lane == 0) write_work_counts(wt, u, cnt);
 }
 
 // Generic merge of caller-given lists (one thread per unit): the union of
@@ -262,6 +275,9 @@ __global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
   const int base = wt.lu_off[u];
   const int room = wt.lu_off[u + 1] - base;
   int ns = 0;
+  int pw = wt.lu_work0[u];        // work unit of the next step
+  int pj = 0;                     // its place in that piece
+  const int plen = wt.lu_len[u];  // piece length
   while (ns < room) {
     int head[kUnitBlocks];
     int n = 0x7fffffff;
@@ -291,7 +307,11 @@ __global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
                      static_cast<int>(diag << kStepDiagShift);
     const int2 st = make_int2(pt.tile_tok0[n], info);
     wt.steps[base + ns] = st;
-    note_step(wt, u, ns, st);
+    if (pj < kFirstSteps) wt.rec[pw].first[pj] = st;
+    if (++pj == plen) {  // the next step opens the next piece
+      pj = 0;
+      ++pw;
+    }
     ++ns;
   }
   write_work_counts(wt, u, ns);

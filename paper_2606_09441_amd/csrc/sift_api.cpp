@@ -216,13 +216,20 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
     hp.step_off[k + 1] = hp.step_off[k] + static_cast<int32_t>(unit_cost[k]);
   }
   // Work units.  A query unit lists every tile of its prompt up to its last
-  // M-block, so its list length is its cost; it is cut into pieces of at
-  // most `piece` steps so that no workgroup walks a list much longer than a
-  // document unit's.  The piece length doubles until at most kMaxSlots
-  // partial slots are needed.
+  // M-block, so its list length is its cost.  The launch runs the longest
+  // work units first (see WorkRec), so a unit only delays the end when it is
+  // longer than the work per workgroup slot; a query unit is cut into pieces
+  // of at most `piece` steps, piece = that work's lower bound (the query
+  // units' steps plus one diagonal step per document M-block, over
+  // kSlots resident workgroups), at least kMinPiece.  The piece length
+  // doubles until at most kMaxSlots partial slots are needed.
   constexpr int64_t kMaxSlots = 4096;
+  constexpr int64_t kMinPiece = 32;
+  constexpr int64_t kSlots = 512;  // 256 CUs x 2 resident attention workgroups
   auto is_query = [&](int64_t k) { return hp.seg_kind[hp.tile_seg[hp.unit_m0[k]]] == sift::kQuery; };
-  int64_t piece = 32;
+  int64_t lower = 0;
+  for (int64_t k = 0; k < U; ++k) lower += is_query(k) ? unit_cost[k] : hp.unit_nb[k];
+  int64_t piece = std::max<int64_t>(kMinPiece, (lower + kSlots - 1) / kSlots);
   auto slots_for = [&](int64_t pc) {
     int64_t n = 0;
     for (int64_t k = 0; k < U; ++k)

@@ -64,7 +64,8 @@ __device__ __forceinline__ int32_t kv_row0(const PlanTables& pt, const KvPages& 
 // Every work unit has a 64-byte record that holds all a workgroup needs
 // before its first K/V fetch, so the kernel's start is one scalar load deep.
 // rec[w] (work units in locality order) is the planner's static part plus
-// the step count and first kFirstSteps steps, written by decode.
+// the step count and first kFirstSteps steps, written by decode (for a split
+// unit, once its whole list is written).
 //
 // Launch order.  Workgroups are dealt round-robin over the kNumXcd XCDs, so
 // workgroup x + kNumXcd * k runs on XCD x.  The locality order is cut into
@@ -126,19 +127,6 @@ struct WorkTables {
   int32_t chunk_size;         // work units per XCD chunk
   int32_t grid;               // kNumXcd * chunk_size
 };
-
-// Step `rel` of list unit u's list, just written: copy it into the record of
-// the piece it opens when it is one of that piece's first kFirstSteps.
-__device__ __forceinline__ void note_step(const WorkTables& wt, int32_t u, int32_t rel, int2 st) {
-  const int32_t nw = wt.lu_nwork[u];
-  int32_t k = 0, j = rel;
-  if (nw > 1) {
-    const int32_t len = wt.lu_len[u];
-    k = rel / len;
-    j = rel - k * len;
-  }
-  if (j < kFirstSteps && k < nw) wt.rec[wt.lu_work0[u] + k].first[j] = st;
-}
 
 // Step counts of a list unit's work units, from the length of its list,
 // and their ranks in their count buckets.

@@ -275,6 +275,21 @@ def test_attention_over_given_lists_matches_plan_run():
         dw.close()
 
 
+def test_attention_over_given_lists_split_units():
+    """The merge of caller-given lists fills the pieces of split query units
+    (llama 4K: each query unit's 66-step list runs as 3 pieces) exactly as
+    decode does."""
+    dw = DevWorkload(workload("llama8b_4k"))
+    try:
+        a = dw.run()
+        rp, ci = dw.plan.decode(dw.la, dw.ca)
+        b = dw.plan.attention(dw.q, dw.k, dw.v, rp, ci)
+        torch.cuda.synchronize()
+        assert torch.equal(a, b)
+    finally:
+        dw.close()
+
+
 def test_plan_decode_then_attention_matches_run():
     wl = workload("llama8b_4k")
     dw = DevWorkload(wl)
