@@ -189,8 +189,9 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   e.ps = wt.lu_off[u];
   e.wt = &wt;
   e.base = e.ps;
+  const int32_t nw = wt.lu_nwork[u], plen = wt.lu_len[u];  // pieces
   e.w0 = wt.lu_work0[u];
-  e.whole = wt.lu_nwork[u] == 1;
+  e.whole = nw == 1;
   e.m0 = m0;
   e.nb = nb;
   e.below = (1ull << lane) - 1ull;
@@ -235,16 +236,16 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   }
   const int32_t cnt = e.ps - e.base;
   if (!e.whole) {
-    // the first steps of every piece, read back from the finished list
-    // (the fence makes this wavefront's stores visible to its loads)
-    __threadfence();
-    const int32_t nw = wt.lu_nwork[u], len = wt.lu_len[u];
+    // the first steps of every piece, read back from the finished list (the
+    // workgroup-scope fence waits for this wavefront's stores, which its
+    // CU's loads then see)
+    __threadfence_block();
     for (int q = lane; q < nw * kFirstSteps; q += 64) {
       const int32_t k = q / kFirstSteps, j = q - k * kFirstSteps;
-      if (k * len + j < cnt) wt.rec[e.w0 + k].first[j] = wt.steps[e.base + k * len + j];
+      if (k * plen + j < cnt) wt.rec[e.w0 + k].first[j] = wt.steps[e.base + k * plen + j];
     }
   }
-  if (lane == 0) write_work_counts(wt, u, cnt);
+  write_work_counts(wt, e.w0, nw, plen, cnt, lane, 64);
 }
 
 // Generic merge of caller-given lists (one thread per unit): the union of
@@ -314,27 +315,23 @@ __global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
     }
     ++ns;
   }
-  write_work_counts(wt, u, ns);
+  write_work_counts(wt, wt.lu_work0[u], wt.lu_nwork[u], plen, ns, 0, 1);
 }
 
-// Schedule pass: block (x, j) places work units j * 256 .. of chunk x at
-// launch[x + kNumXcd * (bucket offset + rank)], after scanning the chunk's
-// kSchedBuckets bucket sizes (4 per thread); the last block to finish
-// clears the buckets.
-__global__ __launch_bounds__(256) void schedule_scatter(WorkTables wt) {
+// Schedule pass, block x for chunk x: scan the chunk's bucket sizes (one
+// bucket per thread) into offsets, clear them, then place every work unit of
+// the chunk at launch[x + kNumXcd * k], k taken from its bucket's offset
+// with an LDS atomic (equal counts land in any order).
+__global__ __launch_bounds__(1024) void schedule_scatter(WorkTables wt) {
   __shared__ int32_t off[kSchedBuckets];
-  __shared__ int32_t wsum[4];
-  __shared__ int32_t last;
+  __shared__ int32_t wsum[16];
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int wave = t >> 6;
-  const int x = blockIdx.y;
-  const int32_t* hist = wt.hist + x * kSchedBuckets;
-  int32_t v[4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) v[k] = hist[4 * t + k];
-  const int32_t own = v[0] + v[1] + v[2] + v[3];
-  int32_t s = own;  // inclusive scan of the thread sums inside the wavefront
+  const int x = blockIdx.x;
+  int32_t* hist = wt.hist + x * kSchedBuckets;
+  const int32_t own = hist[t];
+  int32_t s = own;  // inclusive scan inside the wavefront
   for (int o = 1; o < 64; o <<= 1) {
     const int32_t y = __shfl_up(s, o, 64);
     if (lane >= o) s += y;
@@ -343,40 +340,43 @@ __global__ __launch_bounds__(256) void schedule_scatter(WorkTables wt) {
   __syncthreads();
   int32_t e = s - own;
   for (int j = 0; j < wave; ++j) e += wsum[j];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    off[4 * t + k] = e;
-    e += v[k];
-  }
+  off[t] = e;
+  hist[t] = 0;  // only this block reads the chunk's buckets
   __syncthreads();
-  const int32_t i = blockIdx.x * 256 + t;  // place in the chunk
-  const int32_t w = x * wt.chunk_size + i;
-  if (i < wt.chunk_size && w < wt.num_work) {
-    const int32_t k = off[sched_bucket(wt.rec[w].step_cnt)] + wt.rank[w];
-    if (k >= 0 && k < wt.chunk_size) {
-      const int4* src = reinterpret_cast<const int4*>(wt.rec + w);
-      int4* dst = reinterpret_cast<int4*>(wt.launch + x + kNumXcd * k);
+  // kBatch work units per thread at a time, their loads issued together
+  constexpr int kBatch = 4;
+  const int32_t w_end = min(wt.num_work, (x + 1) * wt.chunk_size);
+  for (int32_t w0 = x * wt.chunk_size; w0 < w_end; w0 += kBatch * 1024) {
+    int4 r[kBatch][4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) dst[q] = src[q];
+    for (int b = 0; b < kBatch; ++b) {
+      const int32_t w = w0 + b * 1024 + t;
+      if (w < w_end) {
+        const int4* src = reinterpret_cast<const int4*>(wt.rec + w);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) r[b][q] = src[q];
+      }
     }
-  }
-  __syncthreads();  // this block's reads of hist are done
-  if (t == 0) {
-    __threadfence();
-    const int32_t nblk = static_cast<int32_t>(gridDim.x * gridDim.y);
-    last = atomicAdd(&wt.hist[kNumXcd * kSchedBuckets], 1) == nblk - 1;
-  }
-  __syncthreads();
-  if (last) {
-    for (int q = t; q <= kNumXcd * kSchedBuckets; q += 256) wt.hist[q] = 0;
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int32_t w = w0 + b * 1024 + t;
+      if (w < w_end) {
+        // the step count is word 9 of the record (rc.y)
+        const int32_t k = atomicAdd(&off[sched_bucket(r[b][2].y)], 1);
+        if (k >= 0 && k < wt.chunk_size) {
+          int4* dst = reinterpret_cast<int4*>(wt.launch + x + kNumXcd * k);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) dst[q] = r[b][q];
+        }
+      }
+    }
   }
 }
 
 hipError_t launch_schedule(const WorkTables& wt, hipStream_t stream) {
   if (wt.num_work == 0) return hipSuccess;
-  hipLaunchKernelGGL(schedule_scatter,
-                     dim3(static_cast<unsigned>((wt.chunk_size + 255) / 256), kNumXcd), dim3(256),
-                     0, stream, wt);
+  static_assert(kSchedBuckets == 1024, "one bucket per thread of the schedule pass");
+  hipLaunchKernelGGL(schedule_scatter, dim3(kNumXcd), dim3(1024), 0, stream, wt);
   return hipGetLastError();
 }
 

@@ -358,9 +358,8 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   const int64_t W = static_cast<int64_t>(hp.wk_head.size());
   const size_t o_steps = align(o_col + std::max<int64_t>(cap, 1) * 4);
   // steps: the units' lists, plus a few entries read (never used) past the end
-  const size_t o_rank = align(o_steps + (std::max<int64_t>(cap, 1) + 8) * 8);
-  const size_t o_hist = align(o_rank + std::max<int64_t>(W, 1) * 4);
-  constexpr size_t kHistBytes = (sift::kNumXcd * sift::kSchedBuckets + 1) * 4;
+  const size_t o_hist = align(o_steps + (std::max<int64_t>(cap, 1) + 8) * 8);
+  constexpr size_t kHistBytes = sift::kNumXcd * sift::kSchedBuckets * 4;
   const size_t o_part_o = align(o_hist + kHistBytes);
   const int64_t slot_rows = hp.part_slots * sift::kUnitRows;
   const size_t o_part_ml = align(o_part_o + slot_rows * head_dim * 4);  // fp32 or bf16 output
@@ -408,7 +407,6 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   plan->pt.num_q_heads = num_q_heads;
   plan->wt.rec = reinterpret_cast<sift::WorkRec*>(P(o_rec));
   plan->wt.launch = reinterpret_cast<sift::WorkRec*>(P(o_launch));
-  plan->wt.rank = P(o_rank);
   plan->wt.hist = P(o_hist);
   plan->wt.lu_head = P(o_uh);
   plan->wt.lu_m0 = P(o_um0);

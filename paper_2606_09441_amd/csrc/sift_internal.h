@@ -3,6 +3,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 namespace sift {
@@ -75,9 +76,10 @@ __device__ __forceinline__ int32_t kv_row0(const PlanTables& pt, const KvPages& 
 // first and the short ones fill the end.  Decode ends with a schedule pass
 // that copies each record to launch[x + kNumXcd * k], k its place in that
 // order (launch slots past a chunk's end hold an empty record: one M-block
-// of no rows, no steps).  The order is a counting sort: decode takes each
-// work unit's rank in its (chunk, count) bucket with an atomic on hist[],
-// and the schedule pass scans hist and scatters (then clears hist).
+// of no rows, no steps).  The order is a counting sort: decode counts the
+// work units of each (chunk, step count) bucket in hist[]; the schedule
+// pass, one block per chunk, scans the chunk's buckets, places each work
+// unit with an LDS atomic on its bucket's offset, and clears the buckets.
 constexpr int kNumXcd = 8;  // MI355X
 constexpr int kUnitBlocks = 2;
 constexpr int kUnitRows = 64 * kUnitBlocks;  // query rows of a unit
@@ -102,13 +104,13 @@ struct alignas(64) WorkRec {
                               // step_cnt are stale)
 };
 static_assert(sizeof(WorkRec) == 64, "one record per 64 bytes");
+static_assert(offsetof(WorkRec, step_cnt) == 36, "the step count is word 9 (read as int4 2, .y)");
 
 struct WorkTables {
   WorkRec* rec;               // [W] locality order (device memory)
   WorkRec* launch;            // [grid] launch order (device scratch, written by the schedule pass)
-  int32_t* rank;              // [W] rank in its (chunk, count) bucket (device scratch)
-  int32_t* hist;              // [kNumXcd * kSchedBuckets + 1] bucket sizes, then a workgroup
-                              // counter (device scratch, zero between decodes)
+  int32_t* hist;              // [kNumXcd * kSchedBuckets] bucket sizes (device scratch, zero
+                              // between decodes)
   // list units (decode)
   const int32_t* lu_head;     // [U]
   const int32_t* lu_m0;       // [U]
@@ -128,16 +130,17 @@ struct WorkTables {
   int32_t grid;               // kNumXcd * chunk_size
 };
 
-// Step counts of a list unit's work units, from the length of its list,
-// and their ranks in their count buckets.
-__device__ __forceinline__ void write_work_counts(const WorkTables& wt, int32_t u, int32_t cnt) {
-  const int32_t w0 = wt.lu_work0[u], nw = wt.lu_nwork[u], len = wt.lu_len[u];
-  for (int32_t k = 0; k < nw; ++k) {
+// Step counts of a list unit's work units w0 .. w0 + nw - 1 (pieces of len
+// steps), from the length of its list, counted in their schedule buckets.
+// Thread `part` of `parts` takes pieces part, part + parts, ...
+__device__ __forceinline__ void write_work_counts(const WorkTables& wt, int32_t w0, int32_t nw,
+                                                  int32_t len, int32_t cnt, int part, int parts) {
+  for (int32_t k = part; k < nw; k += parts) {
     const int32_t rest = cnt - k * len;
     const int32_t c = rest < 0 ? 0 : (rest > len ? len : rest);
     wt.rec[w0 + k].step_cnt = c;
     const int32_t x = (w0 + k) / wt.chunk_size;
-    wt.rank[w0 + k] = atomicAdd(&wt.hist[x * kSchedBuckets + sched_bucket(c)], 1);
+    atomicAdd(&wt.hist[x * kSchedBuckets + sched_bucket(c)], 1);
   }
 }
 
