@@ -247,6 +247,49 @@ sift_status sift_sparse_prefill(const sift_tensor* q, const sift_tensor* k,
                                 const uint8_t* cross_bitmap, int32_t tile,
                                 sift_tensor* out, void* stream);
 
+/*
+ * Offline metadata extraction (Sections 4.1, 4.2; made by a dense
+ * standalone prefill of each document, Section 4.4).
+ *
+ * Each document is prefilled alone: causal softmax(scale * Q K^T) over its
+ * own tokens, per query head (kv head h / (Hq/Hkv)).  With A its
+ * probabilities:
+ *   LA bit of tile (i, j), j <= i: 1 when some causal cell of the tile has
+ *     A > alpha (Section 4.1; the paper uses alpha = 0.001);
+ *   CA bit of key page j: 1 when, over the page's causal cells (query p >= key
+ *     k, k in the page), the number with A > beta exceeds gamma times their
+ *     number (Section 4.2; beta = 0.01, gamma = 0.1).  This is the page
+ *     granular form of the key-column concentration of Section 3.5.
+ * The bits are packed as the online path reads them (see "Bit vectors"
+ * above), for these documents in order: the buffers of a prompt are the
+ * concatenation of its documents' parts.
+ *
+ * sift_extract_sizes: for num_docs documents of lengths
+ *   doc_offsets[d+1] - doc_offsets[d] >= 1 (host, [num_docs + 1],
+ *   doc_offsets[0] == 0), num_q_heads query heads and tile T (16, 32, 64),
+ *   writes the bytes la_out and ca_out must hold and the device workspace
+ *   sift_extract_bits needs.  Any of the three pointers may be NULL.
+ * sift_extract_bits: q [tokens][Hq][D] and k [tokens][Hkv][D] in bf16,
+ *   D 64 or 128, tokens == doc_offsets[num_docs]; alpha, beta >= 0,
+ *   0 <= gamma <= 1; softmax_scale <= 0 means 1/sqrt(D).  la_out, ca_out
+ *   (device) receive the bit vectors; workspace (device, at least the size
+ *   from sift_extract_sizes, 256-byte aligned) is scratch owned by the
+ *   caller.  The call waits for `stream`, uploads its tables to the workspace
+ *   synchronously, then enqueues the kernels on `stream` and returns.
+ *   Calls that share a workspace must be ordered.
+ * Errors: SIFT_E_NULL, SIFT_E_LAYOUT (offsets), SIFT_E_SHAPE (tensors vs
+ *   offsets, Hq % Hkv), SIFT_E_UNSUPPORTED (dtype, D, T, thresholds),
+ *   SIFT_E_CAPACITY (workspace too small), SIFT_E_HIP.
+ */
+sift_status sift_extract_sizes(int32_t num_docs, const int32_t* doc_offsets,
+                               int32_t num_q_heads, int32_t tile, size_t* la_bytes,
+                               size_t* ca_bytes, size_t* workspace_bytes);
+sift_status sift_extract_bits(const sift_tensor* q, const sift_tensor* k, int32_t num_docs,
+                              const int32_t* doc_offsets, int32_t tile, double alpha,
+                              double beta, double gamma, float softmax_scale,
+                              uint8_t* la_out, uint8_t* ca_out, void* workspace,
+                              size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -9,9 +9,12 @@ from ._lib import (  # noqa: F401
     Plan,
     SiftError,
     default_scale,
+    extract_bits,
+    extract_sizes,
     header_functions,
     lib,
     sparse_prefill,
 )
 
-__all__ = ["Plan", "SiftError", "sparse_prefill", "lib", "header_functions", "default_scale"]
+__all__ = ["Plan", "SiftError", "sparse_prefill", "extract_bits", "extract_sizes", "lib",
+           "header_functions", "default_scale"]

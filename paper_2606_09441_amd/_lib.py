@@ -75,6 +75,13 @@ _SIGS = {
     "sift_sparse_prefill": (ctypes.c_int, [ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftTensor),
                                            ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftLayout),
                                            _P, _P, ctypes.c_int32, ctypes.POINTER(SiftTensor), _P]),
+    "sift_extract_sizes": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, ctypes.c_int32,
+                                          ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t),
+                                          ctypes.POINTER(ctypes.c_size_t)]),
+    "sift_extract_bits": (ctypes.c_int, [ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftTensor),
+                                         ctypes.c_int32, _P, ctypes.c_int32, ctypes.c_double,
+                                         ctypes.c_double, ctypes.c_double, ctypes.c_float, _P, _P, _P,
+                                         ctypes.c_size_t, _P]),
 }
 
 _lib = None
@@ -263,6 +270,40 @@ def sparse_prefill(q, k, v, seg_offsets, prompt_seg_ptr, la, ca, tile=64, out=No
         ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), ctypes.byref(lay), _ptr(la), _ptr(ca),
         tile, ctypes.byref(od), _stream_ptr(stream)))
     return out
+
+
+def extract_sizes(doc_offsets, num_q_heads, tile):
+    """(LA bytes, CA bytes, workspace bytes) of sift_extract_bits."""
+    import numpy as np
+    offs = np.ascontiguousarray(np.asarray(doc_offsets, dtype=np.int32))
+    la, ca, ws = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
+    check("sift_extract_sizes", lib().sift_extract_sizes(
+        len(offs) - 1, offs.ctypes.data_as(_P), num_q_heads, tile, ctypes.byref(la), ctypes.byref(ca),
+        ctypes.byref(ws)))
+    return la.value, ca.value, ws.value
+
+
+def extract_bits(q, k, doc_offsets, tile=64, alpha=0.001, beta=0.01, gamma=0.1, scale=None,
+                 workspace=None, stream=None):
+    """Offline metadata of documents prefilled alone (sift_extract_bits).
+
+    q [tokens, Hq, D] and k [tokens, Hkv, D] are bf16 on the GPU; doc_offsets
+    (host, [N+1]) delimit the documents.  Returns (la, ca) uint8 device
+    tensors in the layout the online path reads."""
+    import numpy as np
+    torch = _torch()
+    offs = np.ascontiguousarray(np.asarray(doc_offsets, dtype=np.int32))
+    la_n, ca_n, ws_n = extract_sizes(offs, q.shape[1], tile)
+    la = torch.empty(max(la_n, 1), dtype=torch.uint8, device=q.device)
+    ca = torch.empty(max(ca_n, 1), dtype=torch.uint8, device=q.device)
+    if workspace is None or workspace.numel() < ws_n:
+        workspace = torch.empty(max(ws_n, 1), dtype=torch.uint8, device=q.device)
+    qd, kd = tensor_desc(q), tensor_desc(k)
+    check("sift_extract_bits", lib().sift_extract_bits(
+        ctypes.byref(qd), ctypes.byref(kd), len(offs) - 1, offs.ctypes.data_as(_P), tile,
+        float(alpha), float(beta), float(gamma), ctypes.c_float(0.0 if scale is None else scale),
+        _ptr(la), _ptr(ca), _ptr(workspace), workspace.numel(), _stream_ptr(stream)))
+    return la[:la_n], ca[:ca_n]
 
 
 def default_scale(head_dim: int) -> float:

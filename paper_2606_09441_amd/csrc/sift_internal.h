@@ -178,4 +178,37 @@ hipError_t launch_attn_bf16(const PlanTables& pt, const WorkTables& wt, const At
                             hipStream_t stream);
 hipError_t launch_attn_f32(const PlanTables& pt, const AttnArgs& a, hipStream_t stream);
 
+// Offline extraction (extract.hip).  One record per document; the bit-vector
+// offsets are those of the online path's buffers (document-major, query heads
+// inside), the flag and count offsets index the extraction workspace.
+struct ExtractDoc {
+  int32_t tok0;      // first token on the packed axis
+  int32_t len;       // tokens
+  int32_t P;         // pages, ceil(len / T)
+  int32_t pad;
+  int64_t la_off;    // byte offset of head 0's LA vector
+  int64_t ca_off;    // byte offset of head 0's CA vector
+  int64_t flag_off;  // first tile flag (bytes, Hq * P(P+1)/2 per document)
+  int64_t cnt_off;   // first page count (int32, Hq * P per document)
+};
+
+struct ExtractArgs {
+  const ExtractDoc* docs;
+  const int2* blocks;       // {document, 128-row query block}, longest first
+  const __bf16* q;          // [tokens][hq][D]
+  const __bf16* k;          // [tokens][hkv][D]
+  uint8_t* flags;
+  int32_t* counts;
+  int32_t hq, hkv;
+  float c;                  // softmax scale * log2(e)
+  float log2_alpha, log2_beta;
+  double gamma;
+};
+
+// Zeroes zero_words_n words at zero_base (the flags and counts), runs the
+// extraction over num_blocks query blocks x hq heads, then packs the bits.
+hipError_t launch_extract(const ExtractArgs& a, int32_t num_docs, int32_t num_blocks,
+                          int32_t head_dim, int32_t tile, uint32_t* zero_base, int64_t zero_words_n,
+                          uint8_t* la, uint8_t* ca, hipStream_t stream);
+
 }  // namespace sift

@@ -14,7 +14,7 @@ def test_library_loads_and_exports_every_declared_symbol():
     L = B.lib()
     names = B.header_functions()
     assert "sift_sparse_prefill" in names and "sift_decode_tiles" in names
-    assert len(names) == 11
+    assert len(names) == 13
     for n in names:
         assert hasattr(L, n), n
     # the binding declares every one of them too
@@ -78,3 +78,32 @@ def test_plan_create_rejects_bad_layouts_on_the_host():
     assert B.lib().sift_plan_create(None, 4, 2, 128, 64, ctypes.byref(h)) == 1
     assert B.lib().sift_plan_destroy(None) == 0
     assert B.lib().sift_plan_run_paged(None, None, None, None, None, None, None, 0.0, None, None) == 1
+
+
+def test_extract_sizes_and_argument_checks_on_the_host():
+    # two documents of 64 and 36 tokens, T = 16: 4 and 3 pages, 10 and 6 LA
+    # bits, per query head (Section 4.3 sizes)
+    la, ca, ws = B.extract_sizes([0, 64, 100], 2, 16)
+    assert (la, ca) == (2 * 2 + 2 * 1, 2 * 1 + 2 * 1) and ws > 0
+    L = B.lib()
+    offs = np.array([0, 64, 100], dtype=np.int32)
+    op = offs.ctypes.data_as(ctypes.c_void_p)
+
+    def call(q, k, offs_p=op, n=2, tile=16, alpha=0.001, beta=0.01, gamma=0.1, la=1, ca=1, ws=256,
+             ws_bytes=1 << 30):
+        return L.sift_extract_bits(ctypes.byref(q), ctypes.byref(k), n, offs_p, tile, alpha, beta,
+                                   gamma, 0.0, ctypes.c_void_p(la), ctypes.c_void_p(ca),
+                                   ctypes.c_void_p(ws), ws_bytes, None)
+
+    q, k = _t(100, 2, 128), _t(100, 1, 128)
+    assert call(q, k, offs_p=None) == 1
+    assert call(_t(101, 2, 128), k) == 2                      # tokens vs offsets
+    assert call(q, _t(100, 3, 128)) == 2                      # Hq % Hkv
+    assert call(q, k, tile=48) == 4
+    assert call(_t(100, 2, 128, B.SIFT_F32), _t(100, 1, 128, B.SIFT_F32)) == 4   # bf16 only
+    assert call(_t(100, 2, 96), _t(100, 1, 96)) == 4
+    assert call(q, k, gamma=1.5) == 4 and call(q, k, alpha=-1.0) == 4
+    assert call(q, k, ws_bytes=16) == 5                       # workspace too small
+    assert call(q, k, la=0) == 1
+    bad = np.array([0, 64, 64], dtype=np.int32)               # an empty document
+    assert call(q, k, offs_p=bad.ctypes.data_as(ctypes.c_void_p)) == 3
