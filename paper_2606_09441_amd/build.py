@@ -25,7 +25,7 @@ SOURCES = ["decode.hip", "attn_bf16.hip", "attn_f32.hip", "extract.hip", "sift_a
 # Per-source extra flags.  The bf16 attention kernel takes row maxima of MFMA
 # results that are finite or -inf (masked): NaN canonicalisation around
 # fmaxf would only add instructions, so NaNs are not honoured there.
-EXTRA = {"attn_bf16.hip": ["-fno-honor-nans"]}
+EXTRA = {"attn_bf16.hip": ["-fno-honor-nans"], "extract.hip": ["-fno-honor-nans"]}
 
 ARCH = "gfx950"
 COMMON = [

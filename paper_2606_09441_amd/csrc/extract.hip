@@ -94,9 +94,11 @@ __device__ __forceinline__ void scores(const __bf16* lds, const bf16x8 (&qf)[D /
 }
 
 template <int D, int T>
-__global__ __launch_bounds__(256) void extract_kernel(ExtractArgs a) {
+__global__ __launch_bounds__(256, 3) void extract_kernel(ExtractArgs a) {
   constexpr int kKS = D / 16;
-  __shared__ __attribute__((aligned(16))) __bf16 lds[kKB * D];
+  // two K blocks: block kb is read from slot kb & 1 while block kb + 1 is
+  // written to the other, one barrier per block
+  __shared__ __attribute__((aligned(16))) __bf16 lds[2][kKB * D];
 
   const int2 bl = a.blocks[blockIdx.x];  // {document, query block}, longest first
   const ExtractDoc dc = a.docs[bl.x];
@@ -127,39 +129,55 @@ __global__ __launch_bounds__(256) void extract_kernel(ExtractArgs a) {
   const __bf16* kdoc = a.k + static_cast<int64_t>(dc.tok0) * kstride + static_cast<int64_t>(kvh) * D;
   const float c = a.c;
 
-  auto valid = [&](int kg) { return kg <= p && p < L; };  // kg <= p < L implies kg < L
+  // Cells outside the causal triangle or the document become -inf (their
+  // exponential is 0 and they pass no threshold).  A block is full for a
+  // wavefront when all its keys precede the wavefront's first row and all
+  // its rows are in the document: then nothing is masked.
+  auto mask = [&](f32x16 (&s)[2], int kb) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int kg = kb * kKB + key_of(t, j, hf);
+        if (!(kg <= p && p < L)) s[t][j] = -INFINITY;
+      }
+  };
+  auto full = [&](int kb) { return kb * kKB + kKB - 1 <= row0 && row0 + 31 < L; };
 
   // ---- pass 1: row max and row sum (log2 domain)
   float m = -INFINITY, l = 0.f;
   KLoader<D> ld;
   ld.fetch(kdoc, kstride, min(kKB, L));
+  ld.store(lds[0]);
+  __syncthreads();
   for (int kb = 0; kb < nkb; ++kb) {
-    __syncthreads();  // the previous block's reads are done
-    ld.store(lds);
+    const bool more = kb + 1 < nkb;
+    if (more) ld.fetch(kdoc + static_cast<int64_t>(kb + 1) * kKB * kstride, kstride,
+                       min(kKB, L - (kb + 1) * kKB));
+    if (kb * kKB <= wave_last) {  // else no causal cell for this wavefront
+      f32x16 s[2];
+      scores<D>(lds[kb & 1], qf, l32, hf, s);
+      if (!full(kb)) mask(s, kb);
+      float mx = -INFINITY;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[t][j]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mn = fmaxf(m, mx * c);
+      // mn == -inf: no key yet (lanes past the document's end)
+      const float mb = mn == -INFINITY ? 0.f : mn;
+      float sum = 0.f;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) sum += __builtin_amdgcn_exp2f(s[t][j] * c - mb);
+      sum += __shfl_xor(sum, 32, 64);
+      l = l * __builtin_amdgcn_exp2f(m - mb) + sum;
+      m = mn;
+    }
+    if (more) ld.store(lds[(kb + 1) & 1]);
     __syncthreads();
-    if (kb + 1 < nkb) ld.fetch(kdoc + static_cast<int64_t>(kb + 1) * kKB * kstride, kstride,
-                               min(kKB, L - (kb + 1) * kKB));
-    if (kb * kKB > wave_last) continue;  // no causal cell for this wavefront
-    f32x16 s[2];
-    scores<D>(lds, qf, l32, hf, s);
-    float mx = -INFINITY;
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int j = 0; j < 16; ++j)
-        if (valid(kb * kKB + key_of(t, j, hf))) mx = fmaxf(mx, s[t][j]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float mn = fmaxf(m, mx * c);
-    if (mn == -INFINITY) continue;  // no key yet (lanes past the document's end)
-    float sum = 0.f;
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int j = 0; j < 16; ++j)
-        if (valid(kb * kKB + key_of(t, j, hf))) sum += exp2f(s[t][j] * c - mn);
-    sum += __shfl_xor(sum, 32, 64);
-    l = l * exp2f(m - mn) + sum;
-    m = mn;
   }
 
   // ---- pass 2: decisions.  A > t  <=>  S > (log2 t + log2 l + m) / c
@@ -170,60 +188,61 @@ __global__ __launch_bounds__(256) void extract_kernel(ExtractArgs a) {
   uint8_t* flags = a.flags + dc.flag_off + static_cast<int64_t>(h) * nt;
   int32_t* counts = a.counts + dc.cnt_off + static_cast<int64_t>(h) * dc.P;
   ld.fetch(kdoc, kstride, min(kKB, L));
+  ld.store(lds[0]);
+  __syncthreads();
   for (int kb = 0; kb < nkb; ++kb) {
-    __syncthreads();
-    ld.store(lds);
-    __syncthreads();
-    if (kb + 1 < nkb) ld.fetch(kdoc + static_cast<int64_t>(kb + 1) * kKB * kstride, kstride,
-                               min(kKB, L - (kb + 1) * kKB));
-    if (kb * kKB > wave_last) continue;
-    f32x16 s[2];
-    scores<D>(lds, qf, l32, hf, s);
-    bool qa[4] = {false, false, false, false};  // alpha hit in each 16-key quarter
-    int cnt[4] = {0, 0, 0, 0};                  // beta hits per page of this block
+    const bool more = kb + 1 < nkb;
+    if (more) ld.fetch(kdoc + static_cast<int64_t>(kb + 1) * kKB * kstride, kstride,
+                       min(kKB, L - (kb + 1) * kKB));
+    if (kb * kKB <= wave_last) {
+      f32x16 s[2];
+      scores<D>(lds[kb & 1], qf, l32, hf, s);
+      if (!full(kb)) mask(s, kb);
+      // per 16-key quarter: the lanes with a cell above alpha (a ballot per
+      // register, OR-ed); per page: the cells above beta (ballot popcounts;
+      // both halves of the wavefront hold keys of the same page)
+      unsigned long long qa[4] = {0ull, 0ull, 0ull, 0ull};
+      int cnt[4] = {0, 0, 0, 0};
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const bool v = valid(kb * kKB + key_of(t, j, hf));
-        if (v && s[t][j] > thr_a) qa[2 * t + (j >> 3)] = true;
-        // both halves of the wavefront hold keys of the same page here
-        const int n = __popcll(__ballot(v && s[t][j] > thr_b));
-        cnt[T == 16 ? 2 * t + (j >> 3) : (T == 32 ? t : 0)] += n;
-      }
-    // LA flags: fold the two halves of each quarter's ballot onto 32 queries
-    uint32_t f[4];
+        for (int j = 0; j < 16; ++j) {
+          qa[2 * t + (j >> 3)] |= __ballot(s[t][j] > thr_a);
+          cnt[T == 16 ? 2 * t + (j >> 3) : (T == 32 ? t : 0)] += __popcll(__ballot(s[t][j] > thr_b));
+        }
+      // LA flags: fold the two halves of each quarter's ballot onto 32 queries
+      uint32_t f[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const unsigned long long b = __ballot(qa[q]);
-      f[q] = static_cast<uint32_t>(b) | static_cast<uint32_t>(b >> 32);
-    }
-    if (lane == 0) {
-      if constexpr (T == 16) {
+      for (int q = 0; q < 4; ++q) f[q] = static_cast<uint32_t>(qa[q]) | static_cast<uint32_t>(qa[q] >> 32);
+      if (lane == 0) {
+        if constexpr (T == 16) {
 #pragma unroll
-        for (int r = 0; r < 2; ++r) {
-          const int ti = row0 / 16 + r;
+          for (int r = 0; r < 2; ++r) {
+            const int ti = row0 / 16 + r;
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int tj = kb * 4 + q;
-            if (((f[q] >> (16 * r)) & 0xffffu) && tj <= ti) flags[ti * (ti + 1) / 2 + tj] = 1;
+            for (int q = 0; q < 4; ++q) {
+              const int tj = kb * 4 + q;
+              if (((f[q] >> (16 * r)) & 0xffffu) && tj <= ti) flags[ti * (ti + 1) / 2 + tj] = 1;
+            }
           }
+        } else if constexpr (T == 32) {
+          const int ti = row0 / 32;
+          for (int q = 0; q < 2; ++q) {
+            const int tj = kb * 2 + q;
+            if ((f[2 * q] | f[2 * q + 1]) && tj <= ti) flags[ti * (ti + 1) / 2 + tj] = 1;
+          }
+        } else {
+          const int ti = row0 / 64;
+          if ((f[0] | f[1] | f[2] | f[3]) && kb <= ti) flags[ti * (ti + 1) / 2 + kb] = 1;
         }
-      } else if constexpr (T == 32) {
-        const int ti = row0 / 32;
-        for (int q = 0; q < 2; ++q) {
-          const int tj = kb * 2 + q;
-          if ((f[2 * q] | f[2 * q + 1]) && tj <= ti) flags[ti * (ti + 1) / 2 + tj] = 1;
-        }
-      } else {
-        const int ti = row0 / 64;
-        if ((f[0] | f[1] | f[2] | f[3]) && kb <= ti) flags[ti * (ti + 1) / 2 + kb] = 1;
-      }
-      constexpr int kPages = kKB / T;
+        constexpr int kPages = kKB / T;
 #pragma unroll
-      for (int q = 0; q < kPages; ++q)
-        if (cnt[q] > 0) atomicAdd(&counts[kb * kPages + q], cnt[q]);
+        for (int q = 0; q < kPages; ++q)
+          if (cnt[q] > 0) atomicAdd(&counts[kb * kPages + q], cnt[q]);
+      }
     }
+    if (more) ld.store(lds[(kb + 1) & 1]);
+    __syncthreads();
   }
 }
 
