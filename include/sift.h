@@ -123,7 +123,8 @@ const char* sift_status_string(int32_t status);
  *   layout           host layout, read only during the call
  *   num_q_heads      Hq >= 1;  num_kv_heads: Hkv >= 1, Hq % Hkv == 0
  *   head_dim         D: 64 or 128
- *   tile             T: 16, 32 or 64
+ *   tile             T: 16, 32, 64 or 128 (bf16 attention: 64 or 128;
+ *                    fp32 attention: 16, 32 or 64)
  *   plan_out         receives the plan; the caller frees it with
  *                    sift_plan_destroy.
  * Errors: SIFT_E_NULL, SIFT_E_LAYOUT, SIFT_E_SHAPE, SIFT_E_UNSUPPORTED,
@@ -266,7 +267,7 @@ sift_status sift_sparse_prefill(const sift_tensor* q, const sift_tensor* k,
  *
  * sift_extract_sizes: for num_docs documents of lengths
  *   doc_offsets[d+1] - doc_offsets[d] >= 1 (host, [num_docs + 1],
- *   doc_offsets[0] == 0), num_q_heads query heads and tile T (16, 32, 64),
+ *   doc_offsets[0] == 0), num_q_heads query heads and tile T (16, 32, 64, 128),
  *   writes the bytes la_out and ca_out must hold and the device workspace
  *   sift_extract_bits needs.  Any of the three pointers may be NULL.
  * sift_extract_bits: q [tokens][Hq][D] and k [tokens][Hkv][D] in bf16,

@@ -667,7 +667,8 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanTables pt, WorkTables 
 
 hipError_t launch_attn_bf16(const PlanTables& pt, const WorkTables& wt, const AttnArgs& a,
                             hipStream_t stream) {
-  if (a.tile != kT || a.head_dim != kD) return hipErrorInvalidValue;
+  // T = 128 tiles reach the kernel as 64-row blocks and 64-key steps
+  if ((a.tile != kT && a.tile != 2 * kT) || a.head_dim != kD) return hipErrorInvalidValue;
   if (wt.grid == 0) return hipSuccess;
   if (a.out_f32)
     hipLaunchKernelGGL(attn_bf16_kernel<true>, dim3(wt.grid), dim3(256), 0, stream, pt, wt, a);

@@ -152,17 +152,15 @@ struct Emitter {
       if (on) col[pos[k] + __popcll(mk & below)] = n;
       pos[k] += __popcll(mk);
     }
-    const unsigned long long mu = __ballot(listed != 0u);
-    if (listed != 0u) {
-      const unsigned diag = (n >= m0 && n < m0 + nb) ? 1u << (n - m0) : 0u;
-      const int info = pt->tile_len[n] | static_cast<int>(listed << kStepListedShift) |
-                       static_cast<int>(diag << kStepDiagShift);
-      const int32_t idx = ps + __popcll(mu & below);
-      const int2 st = make_int2(kv_row0(*pt, pages, n), info);
-      steps[idx] = st;
-      if (whole && idx - base < kFirstSteps) wt->rec[w0].first[idx - base] = st;
+    // one or two steps per listed tile, in lane order
+    const TileSteps ts = tile_steps(*pt, pages, n, listed, m0, nb);
+    const unsigned long long mu1 = __ballot(ts.cnt >= 1), mu2 = __ballot(ts.cnt >= 2);
+    const int32_t idx = ps + __popcll(mu1 & below) + __popcll(mu2 & below);
+    for (int q = 0; q < ts.cnt; ++q) {
+      steps[idx + q] = ts.s[q];
+      if (whole && idx + q - base < kFirstSteps) wt->rec[w0].first[idx + q - base] = ts.s[q];
     }
-    ps += __popcll(mu);
+    ps += __popcll(mu1) + __popcll(mu2);
   }
 };
 
@@ -279,7 +277,7 @@ __global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
   int pw = wt.lu_work0[u];        // work unit of the next step
   int pj = 0;                     // its place in that piece
   const int plen = wt.lu_len[u];  // piece length
-  while (ns < room) {
+  while (true) {
     int head[kUnitBlocks];
     int n = 0x7fffffff;
 #pragma unroll
@@ -303,17 +301,17 @@ __global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
         listed |= 1u << k;
         ++it[k];
       }
-    const unsigned diag = (n >= m0 && n < m0 + nb) ? 1u << (n - m0) : 0u;
-    const int info = pt.tile_len[n] | static_cast<int>(listed << kStepListedShift) |
-                     static_cast<int>(diag << kStepDiagShift);
-    const int2 st = make_int2(pt.tile_tok0[n], info);
-    wt.steps[base + ns] = st;
-    if (pj < kFirstSteps) wt.rec[pw].first[pj] = st;
-    if (++pj == plen) {  // the next step opens the next piece
-      pj = 0;
-      ++pw;
+    const TileSteps ts = tile_steps(pt, KvPages{nullptr, 0}, n, listed, m0, nb);
+    if (ns + ts.cnt > room) break;
+    for (int q = 0; q < ts.cnt; ++q) {
+      wt.steps[base + ns] = ts.s[q];
+      if (pj < kFirstSteps) wt.rec[pw].first[pj] = ts.s[q];
+      if (++pj == plen) {  // the next step opens the next piece
+        pj = 0;
+        ++pw;
+      }
+      ++ns;
     }
-    ++ns;
   }
   write_work_counts(wt, wt.lu_work0[u], wt.lu_nwork[u], plen, ns, 0, 1);
 }

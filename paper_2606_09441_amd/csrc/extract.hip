@@ -231,14 +231,21 @@ __global__ __launch_bounds__(256, 3) void extract_kernel(ExtractArgs a) {
             const int tj = kb * 2 + q;
             if ((f[2 * q] | f[2 * q + 1]) && tj <= ti) flags[ti * (ti + 1) / 2 + tj] = 1;
           }
-        } else {
+        } else if constexpr (T == 64) {
           const int ti = row0 / 64;
           if ((f[0] | f[1] | f[2] | f[3]) && kb <= ti) flags[ti * (ti + 1) / 2 + kb] = 1;
+        } else {  // T = 128: the tile spans the workgroup's rows and two key blocks
+          const int ti = row0 / 128, tj = kb / 2;
+          if ((f[0] | f[1] | f[2] | f[3]) && tj <= ti) flags[ti * (ti + 1) / 2 + tj] = 1;
         }
-        constexpr int kPages = kKB / T;
+        if constexpr (T <= kKB) {
+          constexpr int kPages = kKB / T;
 #pragma unroll
-        for (int q = 0; q < kPages; ++q)
-          if (cnt[q] > 0) atomicAdd(&counts[kb * kPages + q], cnt[q]);
+          for (int q = 0; q < kPages; ++q)
+            if (cnt[q] > 0) atomicAdd(&counts[kb * kPages + q], cnt[q]);
+        } else {
+          if (cnt[0] > 0) atomicAdd(&counts[kb / 2], cnt[0]);
+        }
       }
     }
     if (more) ld.store(lds[(kb + 1) & 1]);
@@ -308,11 +315,13 @@ hipError_t launch_extract(const ExtractArgs& a, int32_t num_docs, int32_t num_bl
     if (head_dim == 128) {
       if (tile == 16) launch_extract_dt<128, 16>(a, num_blocks, stream);
       else if (tile == 32) launch_extract_dt<128, 32>(a, num_blocks, stream);
-      else launch_extract_dt<128, 64>(a, num_blocks, stream);
+      else if (tile == 64) launch_extract_dt<128, 64>(a, num_blocks, stream);
+      else launch_extract_dt<128, 128>(a, num_blocks, stream);
     } else {
       if (tile == 16) launch_extract_dt<64, 16>(a, num_blocks, stream);
       else if (tile == 32) launch_extract_dt<64, 32>(a, num_blocks, stream);
-      else launch_extract_dt<64, 64>(a, num_blocks, stream);
+      else if (tile == 64) launch_extract_dt<64, 64>(a, num_blocks, stream);
+      else launch_extract_dt<64, 128>(a, num_blocks, stream);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -30,7 +30,7 @@ sift_status build_extract_plan(int32_t num_docs, const int32_t* offs, int32_t hq
                                ExtractPlan& ep) {
   if (offs == nullptr) return SIFT_E_NULL;
   if (num_docs < 0 || hq < 1) return SIFT_E_LAYOUT;
-  if (tile != 16 && tile != 32 && tile != 64) return SIFT_E_UNSUPPORTED;
+  if (tile != 16 && tile != 32 && tile != 64 && tile != 128) return SIFT_E_UNSUPPORTED;
   if (offs[0] != 0) return SIFT_E_LAYOUT;
   ep.docs.resize(num_docs);
   int64_t la = 0, ca = 0, fl = 0, cn = 0;

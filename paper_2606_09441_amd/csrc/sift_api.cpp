@@ -71,8 +71,8 @@ sift_status check_io(const sift_tensor* q, const sift_tensor* k, const sift_tens
   if ((st = check_tensor(v, tokens, hkv, dim)) != SIFT_OK) return st;
   if ((st = check_tensor(out, tokens, hq, dim)) != SIFT_OK) return st;
   if (q->dtype != k->dtype || q->dtype != v->dtype) return SIFT_E_UNSUPPORTED;
-  if (q->dtype == SIFT_BF16 && (tile != 64 || dim != 128)) return SIFT_E_UNSUPPORTED;
-  if (q->dtype == SIFT_F32 && out->dtype != SIFT_F32) return SIFT_E_UNSUPPORTED;
+  if (q->dtype == SIFT_BF16 && ((tile != 64 && tile != 128) || dim != 128)) return SIFT_E_UNSUPPORTED;
+  if (q->dtype == SIFT_F32 && (out->dtype != SIFT_F32 || tile > 64)) return SIFT_E_UNSUPPORTED;
   return SIFT_OK;
 }
 
@@ -165,10 +165,14 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
     }
   }
 
-  // Attention work units: (query head, M-blocks kUnitBlocks*p .. of a
-  // segment).  The M-blocks of one document share the cross-attention part
-  // of their lists (it depends on the key document only), so a unit stages
-  // each of those key tiles once for all of its query rows.
+  // Attention work units: (query head, M-blocks ub*p .. of a segment).  The
+  // M-blocks of one document share the cross-attention part of their lists
+  // (it depends on the key document only), so a unit stages each of those
+  // key tiles once for all of its query rows.  The bf16 kernel works on
+  // 64-row blocks: up to kUnitBlocks M-blocks of T <= 64 per unit, or one
+  // M-block of T = 128 (two halves, each tile up to two steps).
+  const int32_t halves = tile == 128 ? 2 : 1;
+  const int32_t ub = tile == 128 ? 1 : sift::kUnitBlocks;
   struct Group {
     int32_t m0, nb;
     int64_t cost;  // causal tiles of the group's last M-block: the union's length bound
@@ -176,10 +180,10 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
   std::vector<Group> groups;
   for (int32_t s = 0; s < S; ++s) {
     const int32_t lo = hp.seg_tile0[hp.seg_first[s]];  // first tile of the prompt
-    for (int32_t p = 0; p < hp.seg_pages[s]; p += sift::kUnitBlocks) {
+    for (int32_t p = 0; p < hp.seg_pages[s]; p += ub) {
       const int32_t m0 = hp.seg_tile0[s] + p;
-      const int32_t nb = std::min<int32_t>(sift::kUnitBlocks, hp.seg_pages[s] - p);
-      groups.push_back({m0, nb, m0 + nb - 1 - lo + 1});
+      const int32_t nb = std::min<int32_t>(ub, hp.seg_pages[s] - p);
+      groups.push_back({m0, nb, (m0 + nb - 1 - lo + 1) * halves});
     }
   }
   // Units in locality order: kv head, then longest group first, then the
@@ -271,11 +275,20 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
     sift::WorkRec& r = hp.rec[w];
     r.head = hp.wk_head[w];
     r.kv_head = hp.wk_head[w] / (hq / hkv);
-    r.nb = hp.wk_nb[w];
     r.slot = hp.wk_slot[w];
-    for (int b = 0; b < r.nb; ++b) {
-      r.tok0[b] = hp.tile_tok0[hp.wk_m0[w] + b];
-      r.len[b] = hp.tile_len[hp.wk_m0[w] + b];
+    if (halves == 1) {
+      r.nb = hp.wk_nb[w];
+      for (int b = 0; b < r.nb; ++b) {
+        r.tok0[b] = hp.tile_tok0[hp.wk_m0[w] + b];
+        r.len[b] = hp.tile_len[hp.wk_m0[w] + b];
+      }
+    } else {  // one M-block of T = 128: two kernel blocks of 64 rows
+      const int32_t m = hp.wk_m0[w], len = hp.tile_len[m];
+      r.nb = len > 64 ? 2 : 1;
+      r.tok0[0] = hp.tile_tok0[m];
+      r.len[0] = std::min<int32_t>(len, 64);
+      r.tok0[1] = len > 64 ? hp.tile_tok0[m] + 64 : 0;
+      r.len[1] = len > 64 ? len - 64 : 0;
     }
     r.step_off = hp.wk_off[w];
   }
@@ -322,7 +335,7 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   *plan_out = nullptr;
   if (num_q_heads < 1 || num_kv_heads < 1 || num_q_heads % num_kv_heads != 0) return SIFT_E_SHAPE;
   if (head_dim != 64 && head_dim != 128) return SIFT_E_UNSUPPORTED;
-  if (tile != 16 && tile != 32 && tile != 64) return SIFT_E_UNSUPPORTED;
+  if (tile != 16 && tile != 32 && tile != 64 && tile != 128) return SIFT_E_UNSUPPORTED;
   HostPlan hp;
   sift_status st = build_host_plan(layout, num_q_heads, num_kv_heads, tile, hp);
   if (st != SIFT_OK) return st;
@@ -358,7 +371,10 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   const int64_t W = static_cast<int64_t>(hp.wk_head.size());
   const size_t o_steps = align(o_col + std::max<int64_t>(cap, 1) * 4);
   // steps: the units' lists, plus a few entries read (never used) past the end
-  const size_t o_hist = align(o_steps + (std::max<int64_t>(cap, 1) + 8) * 8);
+  // (the lists' total length bound: one step per listed tile at T <= 64, up
+  // to two at T = 128)
+  const int64_t step_cap = hp.step_off.empty() ? 0 : hp.step_off.back();
+  const size_t o_hist = align(o_steps + (std::max<int64_t>(step_cap, 1) + 8) * 8);
   constexpr size_t kHistBytes = sift::kNumXcd * sift::kSchedBuckets * 4;
   const size_t o_part_o = align(o_hist + kHistBytes);
   const int64_t slot_rows = hp.part_slots * sift::kUnitRows;
@@ -403,6 +419,7 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   plan->pt.tile_len = P(o_tile_len);
   plan->pt.tile_lo = P(o_tile_lo);
   plan->pt.tile = tile;
+  plan->pt.halves = tile == 128 ? 2 : 1;
   plan->pt.num_tiles = hp.num_tiles;
   plan->pt.num_q_heads = num_q_heads;
   plan->wt.rec = reinterpret_cast<sift::WorkRec*>(P(o_rec));
@@ -599,8 +616,9 @@ sift_status sift_plan_run_paged(sift_plan* plan, const sift_tensor* q, const sif
   if (in.num_tiles > 0 && num_pages < 1) return SIFT_E_SHAPE;
   if (in.num_tiles > 0 && page_table == nullptr) return SIFT_E_NULL;
   if (q->dtype != k_pages->dtype || q->dtype != v_pages->dtype) return SIFT_E_UNSUPPORTED;
-  if (q->dtype == SIFT_BF16 && (in.tile != 64 || in.head_dim != 128)) return SIFT_E_UNSUPPORTED;
-  if (q->dtype == SIFT_F32 && out->dtype != SIFT_F32) return SIFT_E_UNSUPPORTED;
+  if (q->dtype == SIFT_BF16 && ((in.tile != 64 && in.tile != 128) || in.head_dim != 128))
+    return SIFT_E_UNSUPPORTED;
+  if (q->dtype == SIFT_F32 && (out->dtype != SIFT_F32 || in.tile > 64)) return SIFT_E_UNSUPPORTED;
   if (in.la_bytes > 0 && local_bitmap == nullptr) return SIFT_E_NULL;
   if (in.ca_bytes > 0 && cross_bitmap == nullptr) return SIFT_E_NULL;
   if ((st = check_device(plan)) != SIFT_OK) return st;
@@ -642,7 +660,7 @@ sift_status sift_sparse_prefill(const sift_tensor* q, const sift_tensor* k, cons
   {
     if (q->heads < 1 || k->heads < 1 || q->heads % k->heads != 0) return SIFT_E_SHAPE;
     if (q->head_dim != 64 && q->head_dim != 128) return SIFT_E_UNSUPPORTED;
-    if (tile != 16 && tile != 32 && tile != 64) return SIFT_E_UNSUPPORTED;
+    if (tile != 16 && tile != 32 && tile != 64 && tile != 128) return SIFT_E_UNSUPPORTED;
     HostPlan hp;
     sift_status st0 = build_host_plan(doc_offsets, q->heads, k->heads, tile, hp);
     if (st0 != SIFT_OK) return st0;

@@ -27,6 +27,7 @@ struct PlanTables {
   int32_t num_tiles;          // M
   int32_t num_q_heads;        // Hq
   int32_t tile;               // T
+  int32_t halves;             // T = 128: 2 (each tile is two 64-row/64-key halves); else 1
 };
 
 // Where the K/V rows of a key tile live.  Packed (table == nullptr): tile m
@@ -147,6 +148,46 @@ __device__ __forceinline__ void write_work_counts(const WorkTables& wt, int32_t 
 constexpr int kStepLenMask = 0xff;
 constexpr int kStepListedShift = 8;
 constexpr int kStepDiagShift = 12;
+
+// The steps (64-key blocks of the bf16 kernel) of key tile n for the list
+// unit of M-blocks m0 .. m0 + nb - 1, which list it as `listed` says (bit k:
+// M-block m0 + k).  Bit b of a step's listed / diagonal fields refers to the
+// unit's 64-row kernel block b.  T <= 64: one step, kernel blocks are the
+// M-blocks.  T = 128 (halves == 2, nb == 1): the M-block is two kernel
+// blocks and the tile up to two steps of 64 keys; on the diagonal tile the
+// first key half is the first row half's diagonal and precedes the second
+// row half entirely, the second key half is the second row half's diagonal.
+struct TileSteps {
+  int cnt;
+  int2 s[2];
+};
+
+__device__ __forceinline__ TileSteps tile_steps(const PlanTables& pt, const KvPages& pg, int32_t n,
+                                                unsigned listed, int32_t m0, int32_t nb) {
+  TileSteps t;
+  t.cnt = 0;
+  if (listed == 0u) return t;
+  const int32_t row0 = kv_row0(pt, pg, n);
+  const int32_t len = pt.tile_len[n];
+  if (pt.halves == 1) {
+    const unsigned diag = (n >= m0 && n < m0 + nb) ? 1u << (n - m0) : 0u;
+    t.cnt = 1;
+    t.s[0] = make_int2(row0, len | static_cast<int>(listed << kStepListedShift) |
+                                 static_cast<int>(diag << kStepDiagShift));
+    return t;
+  }
+  const unsigned rows = pt.tile_len[m0] > 64 ? 3u : 1u;  // kernel blocks of the M-block
+  const unsigned d0 = n == m0 ? 1u : 0u;
+  t.cnt = len > 64 ? 2 : 1;
+  t.s[0] = make_int2(row0, min(len, 64) | static_cast<int>(rows << kStepListedShift) |
+                               static_cast<int>(d0 << kStepDiagShift));
+  if (len > 64) {
+    const unsigned r1 = n == m0 ? 2u : rows;
+    t.s[1] = make_int2(row0 + 64, (len - 64) | static_cast<int>(r1 << kStepListedShift) |
+                                      static_cast<int>((d0 << 1) << kStepDiagShift));
+  }
+  return t;
+}
 
 // Decode (Section 5.1): count, scan, write.  The write pass runs per unit and
 // emits its M-blocks' lists and the unit's merged step list.

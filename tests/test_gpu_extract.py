@@ -58,6 +58,8 @@ CASES = [
     (64, 128, [513, 64, 200, 7], 4, 2, 1.0),
     (16, 128, [190, 128], 2, 2, 2.5),
     (64, 64, [1000], 2, 1, 2.0),
+    (128, 128, [300, 129, 64, 1], 4, 2, 1.5),
+    (128, 64, [700, 128], 2, 1, 1.0),
 ]
 
 
