@@ -134,6 +134,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="long64k")
     ap.add_argument("--rho", type=float, default=None)
+    ap.add_argument("--tile", type=int, default=None,
+                    help="tile size of the RAG workloads (64 or 128; default 64)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
@@ -159,6 +161,8 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs the GPU"
     dev = torch.device("cuda:0")
     kw = {} if args.rho is None else {"rho": args.rho}
+    if args.tile is not None:
+        kw["tile"] = args.tile
     t0 = time.time()
     wl = W.make(args.workload, **kw)
     log(f"workload {wl.name}: {wl.tokens} tokens, hq={wl.hq} hkv={wl.hkv} D={wl.d} "
@@ -361,7 +365,7 @@ def main():
             # HBM bytes per launch (rocprofv3 counters), only for the long64k
             # workload they were taken on
             "traffic": measured_traffic() if args.workload == "long64k" and args.rho is None
-                       else None,
+                       and args.tile in (None, 64) else None,
         },
         "cpu_baseline": cpu,
     }

@@ -230,24 +230,27 @@ def _tiny(seed=0, **_):
                      {"rho": 0.3, "docs": lens, "query": 32})
 
 
-def _llama(seed=0, rho=0.2, **_):
+def _llama(seed=0, rho=0.2, tile=64, **_):
     rng = np.random.default_rng(seed)
-    docs, query = _rag_prompt(rng, [512] * 8, 128, 64, 32, 8, 128, rho)
-    return _assemble("llama8b_4k", [(docs, query)], 64, 32, 8, 128, "bf16",
+    docs, query = _rag_prompt(rng, [512] * 8, 128, tile, 32, 8, 128, rho)
+    return _assemble("llama8b_4k" + ("" if tile == 64 else f"_t{tile}"), [(docs, query)], tile, 32,
+                     8, 128, "bf16",
                      {"rho": rho, "docs": [512] * 8, "query": 128})
 
 
-def _mid(seed=0, rho=0.2, **_):
+def _mid(seed=0, rho=0.2, tile=64, **_):
     rng = np.random.default_rng(seed)
-    docs, query = _rag_prompt(rng, [1024] * 16, 256, 64, 32, 8, 128, rho)
-    return _assemble(f"llama8b_16k_rho{rho:g}", [(docs, query)], 64, 32, 8, 128, "bf16",
+    docs, query = _rag_prompt(rng, [1024] * 16, 256, tile, 32, 8, 128, rho)
+    return _assemble(f"llama8b_16k_rho{rho:g}" + ("" if tile == 64 else f"_t{tile}"), [(docs, query)],
+                     tile, 32, 8, 128, "bf16",
                      {"rho": rho, "docs": [1024] * 16, "query": 256})
 
 
-def _long(seed=0, rho=0.15, hq=48, hkv=8, **_):
+def _long(seed=0, rho=0.15, hq=48, hkv=8, tile=64, **_):
     rng = np.random.default_rng(seed)
-    docs, query = _rag_prompt(rng, [2048] * 32, 512, 64, hq, hkv, 128, rho)
-    return _assemble(f"long64k_{hq}x{hkv}_rho{rho:g}", [(docs, query)], 64, hq, hkv, 128, "bf16",
+    docs, query = _rag_prompt(rng, [2048] * 32, 512, tile, hq, hkv, 128, rho)
+    return _assemble(f"long64k_{hq}x{hkv}_rho{rho:g}" + ("" if tile == 64 else f"_t{tile}"),
+                     [(docs, query)], tile, hq, hkv, 128, "bf16",
                      {"rho": rho, "docs": [2048] * 32, "query": 512})
 
 
@@ -290,8 +293,8 @@ CONFIGS = {
 
 
 def make(name: str, seed: int = 0, **kw) -> Workload:
-    """Build a named configuration.  Extra keywords: rho (density knob) for
-    the RAG configs; hq/hkv for long64k."""
+    """Build a named configuration.  Extra keywords: rho (density knob) and
+    tile (64 or 128) for the RAG configs; hq/hkv for long64k."""
     return CONFIGS[name](seed=seed, **kw)
 
 
