@@ -127,6 +127,50 @@ def extract_leg(wl, q, k, dev, args):
             "work": "two QK^T passes over the causal cells, 4*D flop per cell and head"}
 
 
+def layer_leg(wl, plan, la, ca, dev, args):
+    """Per-layer prefill time of one decoder layer of the workload's shape
+    (hidden = Hq D; the MLP of Llama-3.1-8B, 14336 wide for hidden 4096, else
+    3.5 x hidden), random-init weights: the attention block (norm, q/k/v
+    GEMMs, RoPE, decode + attention, o_proj) and the whole layer (with the
+    SwiGLU MLP), over the workload's bits and over all-ones bits (dense
+    causal attention, the paper's full recompute)."""
+    import torch
+
+    import workloads as W
+    from paper_2606_09441_amd.layer import PrefillLayer
+    hidden = wl.hq * wl.d
+    inter = 14336 if hidden == 4096 else int(3.5 * hidden)
+    w = W.layer_weights(hidden, wl.hq, wl.hkv, wl.d, inter, seed=1)
+    layer = PrefillLayer({k: torch.from_numpy(v).to(dev).bfloat16() for k, v in w.items()},
+                         wl.hq, wl.hkv, wl.d, torch.from_numpy(W.rope_inv_freq(wl.d)).to(dev))
+    x = torch.from_numpy(W.layer_input(wl.tokens, hidden, seed=2)).to(dev).bfloat16()
+    pos = torch.from_numpy(W.prompt_positions(wl.seg_offsets, wl.prompt_seg_ptr)).to(dev)
+    wd = W.all_ones(wl)
+    la_d, ca_d = torch.from_numpy(wd.la).to(dev), torch.from_numpy(wd.ca).to(dev)
+    res = {"hidden": hidden, "intermediate": inter}
+    n = max(3, args.steps // 2)
+    for tag, bits in (("sparse", (la, ca)), ("dense", (la_d, ca_d))):
+        for part, mlp in (("attention_block", False), ("layer", True)):
+            fn = lambda: layer.forward(x, plan, pos, bits[0], bits[1], mlp=mlp)
+            for _ in range(2):
+                fn()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(n):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            res[f"{part}_ms_{tag}"] = round(e0.elapsed_time(e1) / n, 4)
+    res["attention_block_speedup"] = round(res["attention_block_ms_dense"] /
+                                           res["attention_block_ms_sparse"], 3)
+    res["layer_speedup"] = round(res["layer_ms_dense"] / res["layer_ms_sparse"], 3)
+    log(f"layer (hidden {hidden}): attention block {res['attention_block_ms_sparse']:.3f} vs "
+        f"{res['attention_block_ms_dense']:.3f} ms dense, whole layer {res['layer_ms_sparse']:.3f} vs "
+        f"{res['layer_ms_dense']:.3f} ms dense: {res['layer_speedup']:.2f}x")
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -134,6 +178,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="long64k")
     ap.add_argument("--rho", type=float, default=None)
+    ap.add_argument("--layer", action="store_true",
+                    help="also time the decoder-layer prefill slice, sparse vs dense bits")
+    ap.add_argument("--heads", default=None,
+                    help="HQ,HKV for the long64k workload (default 48,8; 32,8 is Llama-3.1-8B)")
     ap.add_argument("--tile", type=int, default=None,
                     help="tile size of the RAG workloads (64 or 128; default 64)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -163,6 +211,8 @@ def main():
     kw = {} if args.rho is None else {"rho": args.rho}
     if args.tile is not None:
         kw["tile"] = args.tile
+    if args.heads is not None:
+        kw["hq"], kw["hkv"] = (int(x) for x in args.heads.split(","))
     t0 = time.time()
     wl = W.make(args.workload, **kw)
     log(f"workload {wl.name}: {wl.tokens} tokens, hq={wl.hq} hkv={wl.hkv} D={wl.d} "
@@ -287,6 +337,10 @@ def main():
         log(f"paged K/V: step {ms_step_p:.3f} ms ({flops / ms_step_p / 1e9:.1f} TFLOP/s)")
         del kp, vp, tl
 
+    layer = None
+    if args.layer and wl.dtype == "bf16":
+        layer = layer_leg(wl, plan, la, ca, dev, args)
+
     extract = None
     if wl.dtype == "bf16" and not args.no_extract:
         extract = extract_leg(wl, q, k, dev, args)
@@ -356,6 +410,7 @@ def main():
         "dense": dense or None,
         "paged": paged,
         "extract": extract,
+        "layer": layer,
         "roofline": {
             "bound": "mfma",
             "achieved": round(achieved, 2),

@@ -291,6 +291,21 @@ sift_status sift_extract_bits(const sift_tensor* q, const sift_tensor* k, int32_
                               uint8_t* la_out, uint8_t* ca_out, void* workspace,
                               size_t workspace_bytes, void* stream);
 
+/*
+ * Rotary position embedding for the decoder-layer prefill slice (the
+ * Llama-3.1-8B layer of Section 6 around the sparse attention): q
+ * [tokens][Hq][D] and k [tokens][Hkv][D], bf16 in device memory, are rotated
+ * in place, rotate-half form: for i < D/2 and angle a = positions[t] *
+ * inv_freq[i] (fp32 product),
+ *   x[i] <- x[i] cos a - x[i + D/2] sin a,  x[i + D/2] <- x[i + D/2] cos a + x[i] sin a.
+ * positions (device, int32 [tokens]) are each token's index in its prompt;
+ * inv_freq (device, float [D/2]) is the frequency table (base^(-2i/D), or a
+ * rescaled one).  Errors: SIFT_E_NULL, SIFT_E_SHAPE (tokens or head sizes
+ * differ), SIFT_E_UNSUPPORTED (not bf16, odd D), SIFT_E_HIP.
+ */
+sift_status sift_rope(const sift_tensor* q, const sift_tensor* k, const int32_t* positions,
+                      const float* inv_freq, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -13,8 +13,9 @@ from ._lib import (  # noqa: F401
     extract_sizes,
     header_functions,
     lib,
+    rope_,
     sparse_prefill,
 )
 
-__all__ = ["Plan", "SiftError", "sparse_prefill", "extract_bits", "extract_sizes", "lib",
+__all__ = ["Plan", "SiftError", "sparse_prefill", "extract_bits", "extract_sizes", "rope_", "lib",
            "header_functions", "default_scale"]

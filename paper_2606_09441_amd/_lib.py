@@ -75,6 +75,7 @@ _SIGS = {
     "sift_sparse_prefill": (ctypes.c_int, [ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftTensor),
                                            ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftLayout),
                                            _P, _P, ctypes.c_int32, ctypes.POINTER(SiftTensor), _P]),
+    "sift_rope": (ctypes.c_int, [ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftTensor), _P, _P, _P]),
     "sift_extract_sizes": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, ctypes.c_int32,
                                           ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t),
                                           ctypes.POINTER(ctypes.c_size_t)]),
@@ -304,6 +305,14 @@ def extract_bits(q, k, doc_offsets, tile=64, alpha=0.001, beta=0.01, gamma=0.1, 
         float(alpha), float(beta), float(gamma), ctypes.c_float(0.0 if scale is None else scale),
         _ptr(la), _ptr(ca), _ptr(workspace), workspace.numel(), _stream_ptr(stream)))
     return la[:la_n], ca[:ca_n]
+
+
+def rope_(q, k, positions, inv_freq, stream=None):
+    """In-place rotary embedding of bf16 q and k (sift_rope)."""
+    qd, kd = tensor_desc(q), tensor_desc(k)
+    check("sift_rope", lib().sift_rope(ctypes.byref(qd), ctypes.byref(kd), _ptr(positions),
+                                       _ptr(inv_freq), _stream_ptr(stream)))
+    return q, k
 
 
 def default_scale(head_dim: int) -> float:

@@ -21,7 +21,8 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(HERE, "libsift.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["decode.hip", "attn_bf16.hip", "attn_f32.hip", "extract.hip", "sift_api.cpp", "extract_api.cpp"]
+SOURCES = ["decode.hip", "attn_bf16.hip", "attn_f32.hip", "extract.hip", "rope.hip", "sift_api.cpp",
+           "extract_api.cpp", "layer_api.cpp"]
 # Per-source extra flags.  The bf16 attention kernel takes row maxima of MFMA
 # results that are finite or -inf (masked): NaN canonicalisation around
 # fmaxf would only add instructions, so NaNs are not honoured there.

@@ -252,4 +252,9 @@ hipError_t launch_extract(const ExtractArgs& a, int32_t num_docs, int32_t num_bl
                           int32_t head_dim, int32_t tile, uint32_t* zero_base, int64_t zero_words_n,
                           uint8_t* la, uint8_t* ca, hipStream_t stream);
 
+// Rotary position embedding of q [tokens][hq][D] and k [tokens][hkv][D]
+// (bf16, in place), angle = positions[t] * inv_freq[i] (rope.hip).
+hipError_t launch_rope(void* q, int64_t tokens, int hq, void* k, int hkv, int head_dim,
+                       const int32_t* positions, const float* inv_freq, hipStream_t stream);
+
 }  // namespace sift

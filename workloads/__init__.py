@@ -26,7 +26,8 @@ from dataclasses import dataclass, field, replace
 
 import numpy as np
 
-__all__ = ["Workload", "make", "CONFIGS", "all_ones", "bf16_round", "pack_msb"]
+__all__ = ["Workload", "make", "CONFIGS", "all_ones", "bf16_round", "pack_msb", "layer_weights",
+           "layer_input", "rope_inv_freq", "prompt_positions"]
 
 
 @dataclass
@@ -336,3 +337,52 @@ def custom(seg_lens_per_prompt, tile, hq, hkv, d, dtype, seed=0, p_la=0.3, p_ca=
         query = _draw_qkv(rng, ql, hq, hkv, d, dtype == "bf16")
         prompts.append((docs, query))
     return _assemble("custom", prompts, tile, hq, hkv, d, dtype, {"p_la": p_la, "p_ca": p_ca})
+
+
+# ----------------------------------------------------------------------------
+# Inputs of the decoder-layer prefill slice (a Llama-3.1-8B-shaped layer)
+# ----------------------------------------------------------------------------
+
+
+def layer_weights(hidden: int, hq: int, hkv: int, d: int, inter: int, seed: int = 0) -> dict:
+    """Random-init weights of one pre-norm decoder layer, bf16 values in
+    float32 arrays: w_in, w_post [hidden]; Wqkv [(hq + 2 hkv) d, hidden];
+    Wo [hidden, hq d]; Wg, Wu [inter, hidden]; Wd [hidden, inter].  Matrices
+    are N(0, 1/fan_in) so that activations keep unit scale."""
+    rng = np.random.default_rng(seed)
+
+    def mat(rows, cols):
+        return bf16_round((rng.standard_normal((rows, cols)) / math.sqrt(cols)).astype(np.float32))
+
+    return {
+        "w_in": bf16_round((1.0 + 0.1 * rng.standard_normal(hidden)).astype(np.float32)),
+        "w_post": bf16_round((1.0 + 0.1 * rng.standard_normal(hidden)).astype(np.float32)),
+        "Wqkv": mat((hq + 2 * hkv) * d, hidden),
+        "Wo": mat(hidden, hq * d),
+        "Wg": mat(inter, hidden),
+        "Wu": mat(inter, hidden),
+        "Wd": mat(hidden, inter),
+    }
+
+
+def layer_input(tokens: int, hidden: int, seed: int = 0) -> np.ndarray:
+    """Residual-stream input x [tokens, hidden], N(0, 1), bf16 values."""
+    rng = np.random.default_rng(seed + 7919)
+    return bf16_round(rng.standard_normal((tokens, hidden)).astype(np.float32))
+
+
+def rope_inv_freq(d: int, base: float = 500000.0) -> np.ndarray:
+    """The rotary frequency table base^(-2i/d), i < d/2 (float32); 500000 is
+    Llama-3.1's base (its long-context rescaling of the table is not applied)."""
+    return (base ** (-np.arange(0, d, 2, dtype=np.float64) / d)).astype(np.float32)
+
+
+def prompt_positions(seg_offsets, prompt_seg_ptr) -> np.ndarray:
+    """Each token's index within its prompt (int32 [tokens])."""
+    so = np.asarray(seg_offsets, dtype=np.int64)
+    ps = np.asarray(prompt_seg_ptr, dtype=np.int64)
+    pos = np.zeros(int(so[-1]), dtype=np.int32)
+    for b in range(len(ps) - 1):
+        a, z = int(so[ps[b]]), int(so[ps[b + 1]])
+        pos[a:z] = np.arange(z - a, dtype=np.int32)
+    return pos
