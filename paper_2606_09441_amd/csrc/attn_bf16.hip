@@ -92,6 +92,7 @@ __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
 // One step of a unit's merged list (see WorkTables), wave-uniform.
 // Wavefronts 0-1 own the unit's first M-block, 2-3 its second.
 struct Step {
+  unsigned sub;  // T < 64: the sub-tile mask of the step (bit G k + s: M-block k lists key tile s)
   int tok0;  // first token of the key tile
   int info;  // len | listed << 8 | diagonal << 12
   bool valid;
@@ -250,6 +251,37 @@ __device__ __forceinline__ bool needs_mask(const Step& st, int wave) {
   return st.diag(wave) || st.len() < kT;
 }
 
+// T = 64 / kG < 64: a 64-key step holds kG key tiles and a wavefront's 32
+// rows kG / 2 row tiles (T = 32: one, T = 16: two, lanes l32 < 16 and >= 16).
+// Cells of (row tile, key tile) pairs the step's sub-tile mask leaves out
+// become -inf.  Register v of s0 holds key 8 (v / 4) + 4 hf + v % 4, of s1
+// the same + 32: key tile (of 16) 2 a + v / 8, (of 32) a.
+template <int kG>
+__device__ __forceinline__ bool sub_partial(const Step& st, int wave) {
+  if constexpr (kG == 1) return false;
+  constexpr unsigned kRow = (1u << (kG * kG / 2)) - 1u;  // a wavefront's bits
+  return ((st.sub >> (wave * kG * kG / 2)) & kRow) != kRow;
+}
+
+template <int kG>
+__device__ __forceinline__ void mask_sub(f32x16& s0, f32x16& s1, const Step& st, int wave, int l32) {
+  if constexpr (kG == 2) {
+    const unsigned m = (st.sub >> (2 * wave)) & 3u;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      if (!(m & 1u)) s0[v] = -INFINITY;
+      if (!(m & 2u)) s1[v] = -INFINITY;
+    }
+  } else if constexpr (kG == 4) {
+    const unsigned m = (st.sub >> (4 * (2 * wave + (l32 >> 4)))) & 15u;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      if (!((m >> (v >> 3)) & 1u)) s0[v] = -INFINITY;
+      if (!((m >> (2 + (v >> 3))) & 1u)) s1[v] = -INFINITY;
+    }
+  }
+}
+
 // Row max of a score tile (both lane halves of the row agree).
 __device__ __forceinline__ float tile_max(const f32x16& s0, const f32x16& s1) {
   float m0 = fmaxf(s0[0], s1[0]);
@@ -264,11 +296,17 @@ __device__ __forceinline__ float tile_max(const f32x16& s0, const f32x16& s1) {
 
 // Lazy rescale: move the reference max (and rescale O and l) only when the
 // tile's scaled max mxs exceeds it by more than kLazy.
+// kG > 1: rows of one wavefront see different sub-tiles, so a lane can
+// still hold mref = -inf (no key yet) when another grows: its factor is 1,
+// not 2^(-inf - -inf).  At T >= 64 every row of a wavefront sees the same
+// tiles and has a key from its first step on.
+template <int kG = 1>
 __device__ __forceinline__ void rescale(RowState& st, float mxs) {
   const bool grow = mxs > st.mref + kLazy;
   if (__builtin_amdgcn_ballot_w64(grow)) {
     const float mnew = grow ? mxs : st.mref;
-    const float alpha = __builtin_amdgcn_exp2f(st.mref - mnew);
+    float alpha = __builtin_amdgcn_exp2f(st.mref - mnew);
+    if constexpr (kG > 1) alpha = grow ? alpha : 1.f;
     st.mref = mnew;
     st.lsum *= alpha;
 #pragma unroll
@@ -349,7 +387,7 @@ __device__ __forceinline__ void pace_qk() {
   }
 }
 
-template <bool kOutF32>
+template <bool kOutF32, int kG>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTables wt,
                                                            AttnArgs a) {
   // K slot 0, K slot 1, V slot 0, V slot 1 (16 KB each)
@@ -422,6 +460,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
 
   // the unit's merged steps
   const int2* __restrict__ steps = wt.steps + rc.x;
+  const uint32_t* __restrict__ subs = wt.sub + rc.x;  // read only when kG > 1
   const int nsteps = rc.y;
   const int64_t kv_head_off = static_cast<int64_t>(kvh) * kD;
   auto rsrc = [&](const __bf16* base, const Step& s) {
@@ -456,6 +495,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
     // steps past the count carry stale values: make_step marks them invalid
     Step c1 = make_step(make_int2(rd.x, rd.y), nsteps > 1);
     Step c2 = make_step(make_int2(rd.z, rd.w), nsteps > 2);
+    if constexpr (kG > 1) {
+      c0.sub = __builtin_amdgcn_readfirstlane(subs[0]);
+      c1.sub = __builtin_amdgcn_readfirstlane(subs[nsteps > 1 ? 1 : 0]);
+      c2.sub = __builtin_amdgcn_readfirstlane(subs[nsteps > 2 ? 2 : 0]);
+    }
     dma_tile<true>(kdst[0], koff0, rstep, rsrc(kp, c0));
     dma_tile<false>(vdst[0], voff0, rstep, rsrc(vp, c0));
     dma_tile<true>(kdst[1], koff0, rstep, rsrc(kp, c1.valid ? c1 : c0));
@@ -465,8 +509,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
     if (c0.in(wave)) {
       qk_tile(qa, 0, qf, sa0, sa1);
       pace_qk();
-      if (needs_mask(c0, wave)) mask_tile(sa0, sa1, c0, wave, qrow, hf);
-      rescale(rs, tile_max(sa0, sa1) * c);
+      if (needs_mask(c0, wave) || sub_partial<kG>(c0, wave)) {
+        mask_tile(sa0, sa1, c0, wave, qrow, hf);
+        mask_sub<kG>(sa0, sa1, c0, wave, l32);
+      }
+      rescale<kG>(rs, tile_max(sa0, sa1) * c);
     }
     __syncthreads();  // K slot 0 is refilled by step 0
 
@@ -478,6 +525,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
       dma_tile<false>(vdst[par ^ 1], voff0, rstep, rsrc(vp, c1.valid ? c1 : c0));
       dma_tile<true>(kdst[par], koff0, rstep, rsrc(kp, c2.valid ? c2 : c0));
       const int2 raw3 = fetch(t + 3);  // decoded after the DMA wait below
+      unsigned sub3 = 0u;
+      if constexpr (kG > 1) sub3 = subs[t + 3 < nsteps ? t + 3 : 0];
       const bool a0 = c0.in(wave);
       const bool a1 = c1.valid && c1.in(wave);
       // keep the per-read addresses derived inside the step (hoisted out of
@@ -510,13 +559,16 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
         }
         if constexpr (!kA0 && kA1) pace_qk();
         if constexpr (kA1) {
-          if (!a1 || needs_mask(c1, wave)) mask_tile(nx0, nx1, c1, wave, qrow, hf, !a1);
+          if (!a1 || needs_mask(c1, wave) || sub_partial<kG>(c1, wave)) {
+            mask_tile(nx0, nx1, c1, wave, qrow, hf, !a1);
+            mask_sub<kG>(nx0, nx1, c1, wave, l32);
+          }
         }
         float mx = -INFINITY;
         if constexpr (kA0) pv_tile(pva, vso, pb, rs);
         if constexpr (kA1) mx = tile_max(nx0, nx1);
         if constexpr (kA0 && kA1) interleave_pv_max();
-        if constexpr (kA1) rescale(rs, mx * c);
+        if constexpr (kA1) rescale<kG>(rs, mx * c);
       };
       using T = std::true_type;
       using F = std::false_type;
@@ -531,6 +583,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
       c0 = c1;
       c1 = c2;
       c2 = make_step(raw3, t + 3 < nsteps);
+      if constexpr (kG > 1) c2.sub = __builtin_amdgcn_readfirstlane(sub3);
     };
 
     for (int t = 0; t < nsteps; t += 2) {
@@ -629,11 +682,14 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanTables pt, WorkTables 
     const OutT* src = po + static_cast<int64_t>(p) * kUnitRows * kD;
 #pragma unroll
     for (int c = 0; c < kDims / kVec; ++c) {
-      const u32x4 raw = *reinterpret_cast<const u32x4*>(src + c * kVec);
+      // (the elements of a loaded vector are read as themselves or by shifts:
+      // a bit_cast of a vector element compiled to loads of element 0 only)
       if constexpr (kOutF32) {
+        const f32x4 val = *reinterpret_cast<const f32x4*>(src + c * kVec);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc[4 * c + e] += w * __builtin_bit_cast(float, raw[e]);
+        for (int e = 0; e < 4; ++e) acc[4 * c + e] += w * val[e];
       } else {
+        const u32x4 raw = *reinterpret_cast<const u32x4*>(src + c * kVec);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {  // bf16 -> f32 is exact: the high half of the word
           const unsigned u = raw[e];
@@ -647,19 +703,19 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanTables pt, WorkTables 
   OutT* dst = static_cast<OutT*>(a.out) + (static_cast<int64_t>(tok) * a.hq + rp->head) * kD + d0;
 #pragma unroll
   for (int c = 0; c < kDims / kVec; ++c) {
-    u32x4 raw;
     if constexpr (kOutF32) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) raw[e] = __builtin_bit_cast(unsigned, acc[4 * c + e] * inv);
+      *reinterpret_cast<f32x4*>(dst + c * kVec) =
+          f32x4{acc[4 * c] * inv, acc[4 * c + 1] * inv, acc[4 * c + 2] * inv, acc[4 * c + 3] * inv};
     } else {
+      u32x4 raw;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const bf16x2 y = bf16x2{static_cast<__bf16>(acc[8 * c + 2 * e] * inv),
                                 static_cast<__bf16>(acc[8 * c + 2 * e + 1] * inv)};
         raw[e] = __builtin_bit_cast(unsigned, y);
       }
+      *reinterpret_cast<u32x4*>(dst + c * kVec) = raw;
     }
-    *reinterpret_cast<u32x4*>(dst + c * kVec) = raw;
   }
 }
 
@@ -667,13 +723,30 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanTables pt, WorkTables 
 
 hipError_t launch_attn_bf16(const PlanTables& pt, const WorkTables& wt, const AttnArgs& a,
                             hipStream_t stream) {
-  // T = 128 tiles reach the kernel as 64-row blocks and 64-key steps
-  if ((a.tile != kT && a.tile != 2 * kT) || a.head_dim != kD) return hipErrorInvalidValue;
+  // T = 128 tiles reach the kernel as 64-row blocks and 64-key steps, T = 16
+  // and 32 tiles as groups of 4 and 2
+  if ((a.tile != 16 && a.tile != 32 && a.tile != kT && a.tile != 2 * kT) || a.head_dim != kD)
+    return hipErrorInvalidValue;
   if (wt.grid == 0) return hipSuccess;
-  if (a.out_f32)
-    hipLaunchKernelGGL(attn_bf16_kernel<true>, dim3(wt.grid), dim3(256), 0, stream, pt, wt, a);
-  else
-    hipLaunchKernelGGL(attn_bf16_kernel<false>, dim3(wt.grid), dim3(256), 0, stream, pt, wt, a);
+  const int g = a.tile < kT ? kT / a.tile : 1;  // key tiles per 64-key step
+  if (a.out_f32) {
+    if (g == 4)
+      hipLaunchKernelGGL((attn_bf16_kernel<true, 4>), dim3(wt.grid), dim3(256), 0, stream, pt, wt, a);
+    else if (g == 2)
+      hipLaunchKernelGGL((attn_bf16_kernel<true, 2>), dim3(wt.grid), dim3(256), 0, stream, pt, wt, a);
+    else
+      hipLaunchKernelGGL((attn_bf16_kernel<true, 1>), dim3(wt.grid), dim3(256), 0, stream, pt, wt, a);
+  } else {
+    if (g == 4)
+      hipLaunchKernelGGL((attn_bf16_kernel<false, 4>), dim3(wt.grid), dim3(256), 0, stream, pt, wt,
+                         a);
+    else if (g == 2)
+      hipLaunchKernelGGL((attn_bf16_kernel<false, 2>), dim3(wt.grid), dim3(256), 0, stream, pt, wt,
+                         a);
+    else
+      hipLaunchKernelGGL((attn_bf16_kernel<false, 1>), dim3(wt.grid), dim3(256), 0, stream, pt, wt,
+                         a);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || wt.num_splits == 0) return e;
   if (a.out_f32)

@@ -128,7 +128,9 @@ __global__ __launch_bounds__(1024) void decode_scan(const int32_t* __restrict__ 
 // Wave-cooperative emitter of one unit's outputs.  Each call handles up to 64
 // candidate key tiles n (one per lane); bit k of `listed` says M-block m0 + k
 // lists n.  Tiles are appended, in lane order, to the lists of the M-blocks
-// that list them and, once, to the merged step list.
+// that list them, and to the merged step list: at T >= 64 one or two steps
+// per tile (tile_steps); at T < 64 one step per group of G = 64 / T
+// consecutive tiles of a segment that any M-block lists (emit_grouped).
 struct Emitter {
   int32_t* col;
   int2* steps;
@@ -138,20 +140,24 @@ struct Emitter {
   int32_t w0;    // its first work unit
   bool whole;    // not split: the first steps go to w0's record here
   KvPages pages;
-  int32_t pos[kUnitBlocks];  // next write position in each M-block's list
-  int32_t ps;                // next write position in the step list
+  int32_t pos[kMaxListBlocks];  // next write position in each M-block's list
+  int32_t ps;                   // next write position in the step list
   int32_t m0, nb;
   unsigned long long below;
 
-  __device__ __forceinline__ void emit(unsigned listed, int32_t n) {
+  __device__ __forceinline__ void lists(unsigned listed, int32_t n) {
 #pragma unroll
-    for (int k = 0; k < kUnitBlocks; ++k) {
+    for (int k = 0; k < kMaxListBlocks; ++k) {
       if (k >= nb) break;
       const bool on = (listed >> k) & 1u;
       const unsigned long long mk = __ballot(on);
       if (on) col[pos[k] + __popcll(mk & below)] = n;
       pos[k] += __popcll(mk);
     }
+  }
+
+  __device__ __forceinline__ void emit(unsigned listed, int32_t n) {
+    lists(listed, n);
     // one or two steps per listed tile, in lane order
     const TileSteps ts = tile_steps(*pt, pages, n, listed, m0, nb);
     const unsigned long long mu1 = __ballot(ts.cnt >= 1), mu2 = __ballot(ts.cnt >= 2);
@@ -161,6 +167,54 @@ struct Emitter {
       if (whole && idx + q - base < kFirstSteps) wt->rec[w0].first[idx + q - base] = ts.s[q];
     }
     ps += __popcll(mu1) + __popcll(mu2);
+  }
+
+  // T < 64.  The lanes hold tiles local = c0 + lane of one segment of P
+  // tiles (c0 a multiple of 64, so a group never straddles two calls).  The
+  // group's first lane gathers its members' bits and writes the step: the
+  // group's first key row and key count, per kernel block (G M-blocks) the
+  // OR of the listed bits and whether the group is the block's diagonal, and
+  // the sub-tile mask.
+  __device__ __forceinline__ void emit_grouped(unsigned listed, int32_t n, int32_t local, int32_t P,
+                                               int lane) {
+    lists(listed, n);
+    const int G = pt->group;
+    unsigned gl[4];
+    gl[0] = listed;
+#pragma unroll
+    for (int q = 1; q < 4; ++q) {
+      const unsigned x = __shfl_down(listed, q, 64);
+      gl[q] = (q < G && lane + q < 64) ? x : 0u;
+    }
+    unsigned any = 0u;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) any |= gl[q];
+    const bool emits = (local & (G - 1)) == 0 && local < P && any != 0u;
+    const unsigned long long mu = __ballot(emits);
+    if (emits) {
+      const int cnt = min(G, P - local);
+      const int len = (cnt - 1) * pt->tile + pt->tile_len[n + cnt - 1];
+      unsigned lst = 0u, sm = 0u;
+      for (int k = 0; k < nb; ++k)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if ((gl[q] >> k) & 1u) {
+            lst |= 1u << (k / G);
+            sm |= 1u << (G * k + q);
+          }
+      unsigned diag = 0u;
+#pragma unroll
+      for (int b = 0; b < kUnitBlocks; ++b)
+        if (n == m0 + G * b) diag |= 1u << b;
+      const int32_t idx = ps + __popcll(mu & below);
+      const int2 st = make_int2(kv_row0(*pt, pages, n),
+                                len | static_cast<int>(lst << kStepListedShift) |
+                                    static_cast<int>(diag << kStepDiagShift));
+      steps[idx] = st;
+      wt->sub[idx] = sm;
+      if (whole && idx - base < kFirstSteps) wt->rec[w0].first[idx - base] = st;
+    }
+    ps += __popcll(mu);
   }
 };
 
@@ -183,7 +237,7 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   e.pt = &pt;
   e.pages = pages;
 #pragma unroll
-  for (int k = 0; k < kUnitBlocks; ++k) e.pos[k] = k < nb ? row_ptr[r0 + k] : 0;
+  for (int k = 0; k < kMaxListBlocks; ++k) e.pos[k] = k < nb ? row_ptr[r0 + k] : 0;
   e.ps = wt.lu_off[u];
   e.wt = &wt;
   e.base = e.ps;
@@ -195,7 +249,8 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   e.below = (1ull << lane) - 1ull;
   const int s = pt.tile_seg[m0];
   const int mlast = m0 + nb - 1;
-  if (pt.seg_kind[s] == kQuery) {
+  const bool grouped = pt.group > 1;
+  if (pt.seg_kind[s] == kQuery && !grouped) {
     // every tile of the prompt up to the M-block (Section 5.1): M-block m0 +
     // k lists n when n <= m0 + k
     const int lo = pt.tile_lo[m0];
@@ -205,6 +260,18 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
       if (n <= mlast) listed = n < m0 ? all : (all & ~((1u << (n - m0)) - 1u));
       e.emit(listed, n);
     }
+  } else if (pt.seg_kind[s] == kQuery) {
+    // the same, segment by segment so that tile groups stay within one call
+    for (int d = pt.seg_first[s]; d <= s; ++d) {
+      const int last = d < s ? pt.seg_pages[d] - 1 : mlast - pt.seg_tile0[s];
+      for (int c0 = 0; c0 <= last; c0 += 64) {
+        const int j = c0 + lane;
+        const int n = pt.seg_tile0[d] + j;
+        unsigned listed = 0u;
+        if (j <= last) listed = n < m0 ? all : (all & ~((1u << (n - m0)) - 1u));
+        e.emit_grouped(listed, n, j, last + 1, lane);
+      }
+    }
   } else {
     // CA pages of every earlier document: the same for all M-blocks
     for (int d = pt.seg_first[s]; d < s; ++d) {
@@ -213,7 +280,10 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
       for (int c0 = 0; c0 < Pe; c0 += 64) {
         const int b = c0 + lane;
         const bool on = b < Pe && get_bit(cav, b);
-        e.emit(on ? all : 0u, pt.seg_tile0[d] + b);
+        if (grouped)
+          e.emit_grouped(on ? all : 0u, pt.seg_tile0[d] + b, b, Pe, lane);
+        else
+          e.emit(on ? all : 0u, pt.seg_tile0[d] + b);
       }
     }
     // LA rows i .. i+nb-1 of the document's triangle, tiles j = 0 .. i+nb-1;
@@ -225,11 +295,14 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
       const int j = c0 + lane;
       unsigned listed = 0u;
 #pragma unroll
-      for (int k = 0; k < kUnitBlocks; ++k) {
+      for (int k = 0; k < kMaxListBlocks; ++k) {
         const int r = i + k;
         if (k < nb && j <= r && (j == r || get_bit(lav, r * (r + 1) / 2 + j))) listed |= 1u << k;
       }
-      e.emit(listed, pt.seg_tile0[s] + j);
+      if (grouped)
+        e.emit_grouped(listed, pt.seg_tile0[s] + j, j, P, lane);
+      else
+        e.emit(listed, pt.seg_tile0[s] + j);
     }
   }
   const int32_t cnt = e.ps - e.base;
@@ -259,11 +332,12 @@ __global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
   const int m0 = wt.lu_m0[u];
   const int nb = wt.lu_nb[u];
   const int lo = pt.tile_lo[m0];
+  const int G = pt.group;
   const int64_t r0 = static_cast<int64_t>(h) * pt.num_tiles + m0;
   auto clampi = [cap](int64_t x) { return min(cap, max(static_cast<int64_t>(0), x)); };
-  int64_t it[kUnitBlocks], end[kUnitBlocks];
+  int64_t it[kMaxListBlocks], end[kMaxListBlocks];
 #pragma unroll
-  for (int k = 0; k < kUnitBlocks; ++k) {
+  for (int k = 0; k < kMaxListBlocks; ++k) {
     it[k] = 0;
     end[k] = 0;
     if (k < nb) {
@@ -277,12 +351,47 @@ __global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
   int pw = wt.lu_work0[u];        // work unit of the next step
   int pj = 0;                     // its place in that piece
   const int plen = wt.lu_len[u];  // piece length
+  auto put = [&](int2 st, uint32_t sm) {
+    wt.steps[base + ns] = st;
+    if (G > 1) wt.sub[base + ns] = sm;
+    if (pj < kFirstSteps) wt.rec[pw].first[pj] = st;
+    if (++pj == plen) {  // the next step opens the next piece
+      pj = 0;
+      ++pw;
+    }
+    ++ns;
+  };
+  // T < 64: the group being gathered (first tile g0, its segment's tile
+  // count P, the listed bits of each member)
+  int g0 = -1, gP = 0;
+  unsigned gl[4] = {0u, 0u, 0u, 0u};
+  auto flush = [&]() {
+    if (g0 < 0 || ns >= room) return;
+    const int cnt = min(G, gP - (g0 - pt.seg_tile0[pt.tile_seg[g0]]));
+    const int len = (cnt - 1) * pt.tile + pt.tile_len[g0 + cnt - 1];
+    unsigned lst = 0u, sm = 0u;
+    for (int k = 0; k < nb; ++k)
+      for (int q = 0; q < G; ++q)
+        if ((gl[q] >> k) & 1u) {
+          lst |= 1u << (k / G);
+          sm |= 1u << (G * k + q);
+        }
+    unsigned diag = 0u;
+    for (int b = 0; b < kUnitBlocks; ++b)
+      if (g0 == m0 + G * b) diag |= 1u << b;
+    put(make_int2(pt.tile_tok0[g0], len | static_cast<int>(lst << kStepListedShift) |
+                                        static_cast<int>(diag << kStepDiagShift)),
+        sm);
+    g0 = -1;
+    gl[0] = gl[1] = gl[2] = gl[3] = 0u;
+  };
   while (true) {
-    int head[kUnitBlocks];
+    int head[kMaxListBlocks];
     int n = 0x7fffffff;
 #pragma unroll
-    for (int k = 0; k < kUnitBlocks; ++k) {
+    for (int k = 0; k < kMaxListBlocks; ++k) {
       head[k] = 0x7fffffff;
+      if (k >= nb) continue;
       while (it[k] < end[k]) {
         const int x = col[it[k]];
         if (x >= lo && x <= m0 + k) {
@@ -296,23 +405,29 @@ __global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
     if (n == 0x7fffffff) break;
     unsigned listed = 0u;
 #pragma unroll
-    for (int k = 0; k < kUnitBlocks; ++k)
-      if (head[k] == n) {
+    for (int k = 0; k < kMaxListBlocks; ++k)
+      if (k < nb && head[k] == n) {
         listed |= 1u << k;
         ++it[k];
       }
-    const TileSteps ts = tile_steps(pt, KvPages{nullptr, 0}, n, listed, m0, nb);
-    if (ns + ts.cnt > room) break;
-    for (int q = 0; q < ts.cnt; ++q) {
-      wt.steps[base + ns] = ts.s[q];
-      if (pj < kFirstSteps) wt.rec[pw].first[pj] = ts.s[q];
-      if (++pj == plen) {  // the next step opens the next piece
-        pj = 0;
-        ++pw;
+    if (G == 1) {
+      const TileSteps ts = tile_steps(pt, KvPages{nullptr, 0}, n, listed, m0, nb);
+      if (ns + ts.cnt > room) break;
+      for (int q = 0; q < ts.cnt; ++q) put(ts.s[q], 0u);
+    } else {
+      const int sg = pt.tile_seg[n];
+      const int local = n - pt.seg_tile0[sg];
+      const int lead = n - (local & (G - 1));
+      if (lead != g0) {
+        flush();
+        if (ns >= room) break;
+        g0 = lead;
+        gP = pt.seg_pages[sg];
       }
-      ++ns;
+      gl[local & (G - 1)] |= listed;
     }
   }
+  if (G > 1 && ns < room) flush();
   write_work_counts(wt, wt.lu_work0[u], wt.lu_nwork[u], plen, ns, 0, 1);
 }
 

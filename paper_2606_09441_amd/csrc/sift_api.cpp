@@ -71,7 +71,7 @@ sift_status check_io(const sift_tensor* q, const sift_tensor* k, const sift_tens
   if ((st = check_tensor(v, tokens, hkv, dim)) != SIFT_OK) return st;
   if ((st = check_tensor(out, tokens, hq, dim)) != SIFT_OK) return st;
   if (q->dtype != k->dtype || q->dtype != v->dtype) return SIFT_E_UNSUPPORTED;
-  if (q->dtype == SIFT_BF16 && ((tile != 64 && tile != 128) || dim != 128)) return SIFT_E_UNSUPPORTED;
+  if (q->dtype == SIFT_BF16 && dim != 128) return SIFT_E_UNSUPPORTED;
   if (q->dtype == SIFT_F32 && (out->dtype != SIFT_F32 || tile > 64)) return SIFT_E_UNSUPPORTED;
   return SIFT_OK;
 }
@@ -169,10 +169,12 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
   // M-blocks of one document share the cross-attention part of their lists
   // (it depends on the key document only), so a unit stages each of those
   // key tiles once for all of its query rows.  The bf16 kernel works on
-  // 64-row blocks: up to kUnitBlocks M-blocks of T <= 64 per unit, or one
-  // M-block of T = 128 (two halves, each tile up to two steps).
+  // units of two 64-row blocks: 128 / T M-blocks of T <= 64 per unit (G =
+  // 64 / T of them per kernel block), or one M-block of T = 128 (two halves,
+  // each tile up to two steps).
   const int32_t halves = tile == 128 ? 2 : 1;
-  const int32_t ub = tile == 128 ? 1 : sift::kUnitBlocks;
+  const int32_t ub = tile == 128 ? 1 : sift::kUnitRows / tile;
+  const int32_t G = tile < 64 ? 64 / tile : 1;
   struct Group {
     int32_t m0, nb;
     int64_t cost;  // causal tiles of the group's last M-block: the union's length bound
@@ -277,10 +279,14 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
     r.kv_head = hp.wk_head[w] / (hq / hkv);
     r.slot = hp.wk_slot[w];
     if (halves == 1) {
-      r.nb = hp.wk_nb[w];
+      // kernel block b: M-blocks m0 + G b .. m0 + G b + G - 1 of the unit
+      const int32_t m0 = hp.wk_m0[w], nb = hp.wk_nb[w];
+      r.nb = (nb + G - 1) / G;
       for (int b = 0; b < r.nb; ++b) {
-        r.tok0[b] = hp.tile_tok0[hp.wk_m0[w] + b];
-        r.len[b] = hp.tile_len[hp.wk_m0[w] + b];
+        r.tok0[b] = hp.tile_tok0[m0 + G * b];
+        r.len[b] = 0;
+        for (int32_t m = m0 + G * b; m < std::min(m0 + nb, m0 + G * b + G); ++m)
+          r.len[b] += hp.tile_len[m];
       }
     } else {  // one M-block of T = 128: two kernel blocks of 64 rows
       const int32_t m = hp.wk_m0[w], len = hp.tile_len[m];
@@ -374,7 +380,9 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   // (the lists' total length bound: one step per listed tile at T <= 64, up
   // to two at T = 128)
   const int64_t step_cap = hp.step_off.empty() ? 0 : hp.step_off.back();
-  const size_t o_hist = align(o_steps + (std::max<int64_t>(step_cap, 1) + 8) * 8);
+  const size_t o_sub = align(o_steps + (std::max<int64_t>(step_cap, 1) + 8) * 8);
+  // per-step sub-tile masks, T < 64 only
+  const size_t o_hist = align(o_sub + (tile < 64 ? (std::max<int64_t>(step_cap, 1) + 8) * 4 : 0));
   constexpr size_t kHistBytes = sift::kNumXcd * sift::kSchedBuckets * 4;
   const size_t o_part_o = align(o_hist + kHistBytes);
   const int64_t slot_rows = hp.part_slots * sift::kUnitRows;
@@ -420,6 +428,7 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   plan->pt.tile_lo = P(o_tile_lo);
   plan->pt.tile = tile;
   plan->pt.halves = tile == 128 ? 2 : 1;
+  plan->pt.group = tile < 64 ? 64 / tile : 1;
   plan->pt.num_tiles = hp.num_tiles;
   plan->pt.num_q_heads = num_q_heads;
   plan->wt.rec = reinterpret_cast<sift::WorkRec*>(P(o_rec));
@@ -433,6 +442,7 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   plan->wt.lu_nwork = P(o_lnw);
   plan->wt.lu_len = P(o_llen);
   plan->wt.steps = reinterpret_cast<int2*>(P(o_steps));
+  plan->wt.sub = tile < 64 ? reinterpret_cast<uint32_t*>(P(o_sub)) : nullptr;
   plan->wt.splits = reinterpret_cast<const int4*>(P(o_splits));
   plan->wt.part_o = static_cast<void*>(P(o_part_o));
   plan->wt.part_ml = reinterpret_cast<float2*>(P(o_part_ml));
@@ -616,8 +626,8 @@ sift_status sift_plan_run_paged(sift_plan* plan, const sift_tensor* q, const sif
   if (in.num_tiles > 0 && num_pages < 1) return SIFT_E_SHAPE;
   if (in.num_tiles > 0 && page_table == nullptr) return SIFT_E_NULL;
   if (q->dtype != k_pages->dtype || q->dtype != v_pages->dtype) return SIFT_E_UNSUPPORTED;
-  if (q->dtype == SIFT_BF16 && ((in.tile != 64 && in.tile != 128) || in.head_dim != 128))
-    return SIFT_E_UNSUPPORTED;
+  // bf16 pages of T < 64 rows: a 64-key step would span several pages
+  if (q->dtype == SIFT_BF16 && (in.tile < 64 || in.head_dim != 128)) return SIFT_E_UNSUPPORTED;
   if (q->dtype == SIFT_F32 && (out->dtype != SIFT_F32 || in.tile > 64)) return SIFT_E_UNSUPPORTED;
   if (in.la_bytes > 0 && local_bitmap == nullptr) return SIFT_E_NULL;
   if (in.ca_bytes > 0 && cross_bitmap == nullptr) return SIFT_E_NULL;

@@ -28,6 +28,7 @@ struct PlanTables {
   int32_t num_q_heads;        // Hq
   int32_t tile;               // T
   int32_t halves;             // T = 128: 2 (each tile is two 64-row/64-key halves); else 1
+  int32_t group;              // T < 64: 64 / T tiles per 64-row block and per step; else 1
 };
 
 // Where the K/V rows of a key tile live.  Packed (table == nullptr): tile m
@@ -82,8 +83,9 @@ __device__ __forceinline__ int32_t kv_row0(const PlanTables& pt, const KvPages& 
 // pass, one block per chunk, scans the chunk's buckets, places each work
 // unit with an LDS atomic on its bucket's offset, and clears the buckets.
 constexpr int kNumXcd = 8;  // MI355X
-constexpr int kUnitBlocks = 2;
+constexpr int kUnitBlocks = 2;                 // 64-row kernel blocks of a unit
 constexpr int kUnitRows = 64 * kUnitBlocks;  // query rows of a unit
+constexpr int kMaxListBlocks = 8;            // M-blocks of a list unit: 128 / T, at most 8 (T = 16)
 constexpr int kFirstSteps = 3;
 constexpr int kSchedBuckets = 1024;          // step counts >= 1023 share bucket 0
 
@@ -121,6 +123,8 @@ struct WorkTables {
   const int32_t* lu_nwork;    // [U]
   const int32_t* lu_len;      // [U] piece length (a bound of the list when not split)
   int2* steps;                // [lu_off[U]] (device scratch)
+  uint32_t* sub;              // [lu_off[U]] per step, T < 64 only: bit G k + s set when the
+                              // unit's M-block k lists key tile s of the step (device scratch)
   const int4* splits;         // [NS] {record of the first piece, first slot, slots, 0}
   void* part_o;               // [slots][kUnitRows][head_dim], output type (device scratch)
   float2* part_ml;            // [slots][kUnitRows] {reference max, row sum}

@@ -54,7 +54,7 @@ def test_prefill_rejects_bad_arguments_on_the_host():
     # unsupported
     assert _prefill(q, k, k, so, ps, tile=48) == 4
     assert _prefill(_t(160, 4, 96), _t(160, 2, 96), _t(160, 2, 96), so, ps) == 4
-    assert _prefill(q, k, k, so, ps, tile=16) == 4                      # bf16 MFMA path needs T = 64
+    assert _prefill(_t(160, 4, 64), _t(160, 2, 64), _t(160, 2, 64), so, ps) == 4   # bf16 needs D = 128
     q32 = _t(160, 4, 128, B.SIFT_F32)
     assert _prefill(q32, _t(160, 2, 128, B.SIFT_F32), _t(160, 2, 128, B.SIFT_F32), so, ps,
                     out=_t(160, 4, 128, B.SIFT_BF16)) == 4             # fp32 in, bf16 out

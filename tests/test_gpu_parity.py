@@ -275,6 +275,13 @@ def test_attention_over_given_lists_matches_plan_run():
         dw.close()
 
 
+def test_attention_llama4k_fp32_output_split_units():
+    """fp32 output with split query units: the pieces' partials are fp32 and
+    the merge reads them as such (llama 4K: 3 pieces per query unit)."""
+    _full_parity(workload("llama8b_4k"), BF16_TOL, out_dtype=torch.float32, heads=[0, 7, 31],
+                 tag="llama8b_4k fp32 out")
+
+
 def test_attention_over_given_lists_split_units():
     """The merge of caller-given lists fills the pieces of split query units
     (llama 4K: each query unit's 66-step list runs as 3 pieces) exactly as
