@@ -1,0 +1,78 @@
+"""GPU: scores that rise far above the first tiles a row sees.
+
+Section 5.2 keeps the online softmax of dense attention.  The bf16 kernel
+forms a tile's weights against the reference max a row took from its first
+tile and bounds them by their sums; a unit in which some sum exceeds the
+bound (a score far above the reference, or an exp2 overflow) is done again
+with the reference following every tile's max.  Here K rows are scaled up
+along each segment, so that later tiles score 2^30 to 2^200 times the first
+one: every unit fails the check and is redone.  The outputs must still
+match the fp64 oracle, for every tile variant and for split query units."""
+
+import numpy as np
+import pytest
+
+import workloads as W
+from gpu_helpers import BF16_TOL, DevWorkload, max_abs, oracle_layout, say
+from oracle import sift_oracle as O
+
+pytestmark = pytest.mark.gpu
+
+RAGGED = [[300, 64, 129, 75], [5], [1, 64, 0], [200, 131, 70], [17, 33, 49]]
+
+
+def _rising(wl: W.Workload, top: float) -> W.Workload:
+    """K rows scaled from 1 at each segment's first token to `top` at its
+    last, then rounded to bf16 again."""
+    f = np.ones(wl.tokens, np.float64)
+    so = wl.seg_offsets
+    for s in range(len(so) - 1):
+        a, z = int(so[s]), int(so[s + 1])
+        if z > a:
+            f[a:z] = 1.0 + (top - 1.0) * np.arange(z - a) / max(1, z - a - 1)
+    wl.k = W.bf16_round((wl.k * f[:, None, None]).astype(np.float32))
+    return wl
+
+
+def _parity(wl, tag):
+    dw = DevWorkload(wl)
+    try:
+        out = dw.run().float().cpu().numpy()
+    finally:
+        dw.close()
+    ref = O.attention(oracle_layout(wl), wl.q, wl.k, wl.v, wl.la, wl.ca)
+    err = max_abs(out, ref)
+    say(f"[range] {tag}: max-abs {err:.3e} (tol {BF16_TOL:g})")
+    assert np.isfinite(out).all(), tag
+    assert err <= BF16_TOL, tag
+
+
+@pytest.mark.parametrize("tile", [16, 32, 64, 128])
+@pytest.mark.parametrize("top", [30.0, 80.0])
+def test_rising_scores_ragged_layouts(tile, top):
+    wl = _rising(W.custom(RAGGED, tile=tile, hq=4, hkv=2, d=128, dtype="bf16", seed=tile + 5,
+                          p_la=0.5, p_ca=0.4), top)
+    _parity(wl, f"T={tile} K x1..{top:g}")
+
+
+def test_rising_scores_split_query_units():
+    """Eight 512-token documents and a 128-token query: the query units'
+    66-step lists run as pieces, each redone on its own and then merged."""
+    wl = _rising(W.custom([[512] * 8 + [128]], tile=64, hq=4, hkv=1, d=128, dtype="bf16",
+                          seed=21, p_la=0.3, p_ca=0.3), 60.0)
+    _parity(wl, "split query units, K x1..60")
+
+
+def test_falling_and_flat_scores():
+    """Scores that fall along the segment (the first reference stays the
+    max) and all-equal scores (every weight is 1)."""
+    wl = W.custom(RAGGED, tile=64, hq=4, hkv=2, d=128, dtype="bf16", seed=3)
+    f = np.ones(wl.tokens)
+    so = wl.seg_offsets
+    for s in range(len(so) - 1):
+        a, z = int(so[s]), int(so[s + 1])
+        f[a:z] = np.linspace(40.0, 1.0, max(1, z - a))[: z - a]
+    wl.k = W.bf16_round((wl.k * f[:, None, None]).astype(np.float32))
+    _parity(wl, "falling scores")
+    wl.k = np.zeros_like(wl.k)
+    _parity(wl, "flat scores")
