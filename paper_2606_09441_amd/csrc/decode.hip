@@ -131,6 +131,7 @@ __global__ __launch_bounds__(1024) void decode_scan(const int32_t* __restrict__ 
 // that list them, and to the merged step list: at T >= 64 one or two steps
 // per tile (tile_steps); at T < 64 one step per group of G = 64 / T
 // consecutive tiles of a segment that any M-block lists (emit_grouped).
+template <int kNb>  // most M-blocks of a list unit (128 / T, at least 2)
 struct Emitter {
   int32_t* col;
   int2* steps;
@@ -140,14 +141,14 @@ struct Emitter {
   int32_t w0;    // its first work unit
   bool whole;    // not split: the first steps go to w0's record here
   KvPages pages;
-  int32_t pos[kMaxListBlocks];  // next write position in each M-block's list
+  int32_t pos[kNb];  // next write position in each M-block's list
   int32_t ps;                   // next write position in the step list
   int32_t m0, nb;
   unsigned long long below;
 
   __device__ __forceinline__ void lists(unsigned listed, int32_t n) {
 #pragma unroll
-    for (int k = 0; k < kMaxListBlocks; ++k) {
+    for (int k = 0; k < kNb; ++k) {
       if (k >= nb) break;
       const bool on = (listed >> k) & 1u;
       const unsigned long long mk = __ballot(on);
@@ -218,6 +219,10 @@ struct Emitter {
   }
 };
 
+// kNb: the most M-blocks of a list unit (2 at T >= 64, 4 at T = 32, 8 at
+// T = 16); kGrouped: T < 64 (steps are groups of tiles).  Separate
+// instances keep the T >= 64 one free of the wider unit's registers.
+template <int kNb, bool kGrouped>
 __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt,
                                                     const uint8_t* __restrict__ la,
                                                     const uint8_t* __restrict__ ca,
@@ -231,13 +236,13 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   const int nb = wt.lu_nb[u];
   const unsigned all = (1u << nb) - 1u;
   const int64_t r0 = static_cast<int64_t>(h) * pt.num_tiles + m0;
-  Emitter e;
+  Emitter<kNb> e;
   e.col = col;
   e.steps = wt.steps;
   e.pt = &pt;
   e.pages = pages;
 #pragma unroll
-  for (int k = 0; k < kMaxListBlocks; ++k) e.pos[k] = k < nb ? row_ptr[r0 + k] : 0;
+  for (int k = 0; k < kNb; ++k) e.pos[k] = k < nb ? row_ptr[r0 + k] : 0;
   e.ps = wt.lu_off[u];
   e.wt = &wt;
   e.base = e.ps;
@@ -249,7 +254,7 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   e.below = (1ull << lane) - 1ull;
   const int s = pt.tile_seg[m0];
   const int mlast = m0 + nb - 1;
-  const bool grouped = pt.group > 1;
+  constexpr bool grouped = kGrouped;
   if (pt.seg_kind[s] == kQuery && !grouped) {
     // every tile of the prompt up to the M-block (Section 5.1): M-block m0 +
     // k lists n when n <= m0 + k
@@ -260,7 +265,7 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
       if (n <= mlast) listed = n < m0 ? all : (all & ~((1u << (n - m0)) - 1u));
       e.emit(listed, n);
     }
-  } else if (pt.seg_kind[s] == kQuery) {
+  } else if (grouped && pt.seg_kind[s] == kQuery) {
     // the same, segment by segment so that tile groups stay within one call
     for (int d = pt.seg_first[s]; d <= s; ++d) {
       const int last = d < s ? pt.seg_pages[d] - 1 : mlast - pt.seg_tile0[s];
@@ -280,7 +285,7 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
       for (int c0 = 0; c0 < Pe; c0 += 64) {
         const int b = c0 + lane;
         const bool on = b < Pe && get_bit(cav, b);
-        if (grouped)
+        if constexpr (grouped)
           e.emit_grouped(on ? all : 0u, pt.seg_tile0[d] + b, b, Pe, lane);
         else
           e.emit(on ? all : 0u, pt.seg_tile0[d] + b);
@@ -295,11 +300,11 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
       const int j = c0 + lane;
       unsigned listed = 0u;
 #pragma unroll
-      for (int k = 0; k < kMaxListBlocks; ++k) {
+      for (int k = 0; k < kNb; ++k) {
         const int r = i + k;
         if (k < nb && j <= r && (j == r || get_bit(lav, r * (r + 1) / 2 + j))) listed |= 1u << k;
       }
-      if (grouped)
+      if constexpr (grouped)
         e.emit_grouped(listed, pt.seg_tile0[s] + j, j, P, lane);
       else
         e.emit(listed, pt.seg_tile0[s] + j);
@@ -511,8 +516,16 @@ hipError_t launch_decode(const PlanTables& pt, const WorkTables& wt, const uint8
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (wt.num_units == 0) return hipSuccess;
-  hipLaunchKernelGGL(decode_write, dim3(static_cast<unsigned>((wt.num_units + 3) / 4)), dim3(256),
-                     0, stream, pt, wt, la, ca, row_ptr, col_idx, pages);
+  const dim3 wgrid(static_cast<unsigned>((wt.num_units + 3) / 4));
+  if (pt.group == 4)
+    hipLaunchKernelGGL((decode_write<8, true>), wgrid, dim3(256), 0, stream, pt, wt, la, ca, row_ptr,
+                       col_idx, pages);
+  else if (pt.group == 2)
+    hipLaunchKernelGGL((decode_write<4, true>), wgrid, dim3(256), 0, stream, pt, wt, la, ca, row_ptr,
+                       col_idx, pages);
+  else
+    hipLaunchKernelGGL((decode_write<2, false>), wgrid, dim3(256), 0, stream, pt, wt, la, ca,
+                       row_ptr, col_idx, pages);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_schedule(wt, stream);
