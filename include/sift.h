@@ -249,6 +249,35 @@ sift_status sift_sparse_prefill(const sift_tensor* q, const sift_tensor* k,
                                 sift_tensor* out, void* stream);
 
 /*
+ * The one-shot form with the caller's softmax scale and device workspace
+ * (Sections 4 and 5; same computation as sift_sparse_prefill).
+ *
+ * sift_workspace_bytes: the device workspace bytes sift_sparse_prefill_ex
+ *   needs for this layout, head counts, head dimension and tile size (the
+ *   plan's tables and the decode and merge scratch).  Host only.
+ * sift_sparse_prefill_ex: softmax_scale <= 0 means 1/sqrt(D).  workspace
+ *   (device, 256-byte aligned, at least sift_workspace_bytes) is owned by
+ *   the caller; the library allocates no device memory.  The call waits for
+ *   `stream` (earlier work on it may still read the workspace), uploads the
+ *   plan's tables into the workspace, enqueues decode and attention on
+ *   `stream` and returns without waiting for them.  The workspace must stay
+ *   allocated until that work is done; calls sharing a workspace must be on
+ *   one stream or otherwise ordered.
+ * Errors: as sift_sparse_prefill, plus SIFT_E_NULL (no workspace),
+ *   SIFT_E_CAPACITY (too small) and SIFT_E_UNSUPPORTED (misaligned), all
+ *   before anything is enqueued.
+ */
+sift_status sift_workspace_bytes(const sift_layout* layout, int32_t num_q_heads,
+                                 int32_t num_kv_heads, int32_t head_dim, int32_t tile,
+                                 size_t* bytes);
+sift_status sift_sparse_prefill_ex(const sift_tensor* q, const sift_tensor* k,
+                                   const sift_tensor* v, const sift_layout* doc_offsets,
+                                   const uint8_t* local_bitmap,
+                                   const uint8_t* cross_bitmap, int32_t tile,
+                                   float softmax_scale, void* workspace,
+                                   size_t workspace_bytes, sift_tensor* out, void* stream);
+
+/*
  * Offline metadata extraction (Sections 4.1, 4.2; made by a dense
  * standalone prefill of each document, Section 4.4).
  *

@@ -15,7 +15,9 @@ from ._lib import (  # noqa: F401
     lib,
     rope_,
     sparse_prefill,
+    sparse_prefill_ex,
+    workspace_bytes,
 )
 
-__all__ = ["Plan", "SiftError", "sparse_prefill", "extract_bits", "extract_sizes", "rope_", "lib",
+__all__ = ["Plan", "SiftError", "sparse_prefill", "sparse_prefill_ex", "workspace_bytes", "extract_bits", "extract_sizes", "rope_", "lib",
            "header_functions", "default_scale"]

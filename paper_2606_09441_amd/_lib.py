@@ -75,6 +75,13 @@ _SIGS = {
     "sift_sparse_prefill": (ctypes.c_int, [ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftTensor),
                                            ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftLayout),
                                            _P, _P, ctypes.c_int32, ctypes.POINTER(SiftTensor), _P]),
+    "sift_workspace_bytes": (ctypes.c_int, [ctypes.POINTER(SiftLayout), ctypes.c_int32, ctypes.c_int32,
+                                            ctypes.c_int32, ctypes.c_int32,
+                                            ctypes.POINTER(ctypes.c_size_t)]),
+    "sift_sparse_prefill_ex": (ctypes.c_int, [ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftTensor),
+                                              ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftLayout),
+                                              _P, _P, ctypes.c_int32, ctypes.c_float, _P,
+                                              ctypes.c_size_t, ctypes.POINTER(SiftTensor), _P]),
     "sift_rope": (ctypes.c_int, [ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftTensor), _P, _P, _P]),
     "sift_extract_sizes": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, ctypes.c_int32,
                                           ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t),
@@ -270,6 +277,36 @@ def sparse_prefill(q, k, v, seg_offsets, prompt_seg_ptr, la, ca, tile=64, out=No
     check("sift_sparse_prefill", lib().sift_sparse_prefill(
         ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), ctypes.byref(lay), _ptr(la), _ptr(ca),
         tile, ctypes.byref(od), _stream_ptr(stream)))
+    return out
+
+
+def workspace_bytes(seg_offsets, prompt_seg_ptr, num_q_heads, num_kv_heads, head_dim, tile=64):
+    """Device workspace bytes of sparse_prefill_ex (sift_workspace_bytes)."""
+    lay, keep = layout_struct(seg_offsets, prompt_seg_ptr)
+    n = ctypes.c_size_t()
+    check("sift_workspace_bytes", lib().sift_workspace_bytes(
+        ctypes.byref(lay), num_q_heads, num_kv_heads, head_dim, tile, ctypes.byref(n)))
+    return n.value
+
+
+def sparse_prefill_ex(q, k, v, seg_offsets, prompt_seg_ptr, la, ca, tile=64, scale=None,
+                      workspace=None, out=None, stream=None):
+    """One-shot form with the caller's scale and workspace (sift_sparse_prefill_ex):
+    no device allocation in the library; returns once the work is enqueued.
+    workspace: a uint8 device tensor of at least workspace_bytes(...) bytes
+    (allocated here when None)."""
+    torch = _torch()
+    if out is None:
+        out = torch.empty_like(q)
+    if workspace is None:
+        n = workspace_bytes(seg_offsets, prompt_seg_ptr, q.shape[1], k.shape[1], q.shape[2], tile)
+        workspace = torch.empty(max(n, 1), dtype=torch.uint8, device=q.device)
+    lay, keep = layout_struct(seg_offsets, prompt_seg_ptr)
+    qd, kd, vd, od = tensor_desc(q), tensor_desc(k), tensor_desc(v), tensor_desc(out)
+    check("sift_sparse_prefill_ex", lib().sift_sparse_prefill_ex(
+        ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), ctypes.byref(lay), _ptr(la), _ptr(ca),
+        tile, ctypes.c_float(0.0 if scale is None else scale), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), ctypes.byref(od), _stream_ptr(stream)))
     return out
 
 

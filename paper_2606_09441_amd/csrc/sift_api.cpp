@@ -31,6 +31,7 @@ struct sift_plan {
   // one device allocation holds every table, then the decode scratch
   void* dev = nullptr;
   size_t dev_bytes = 0;
+  bool owns_dev = true;  // false: the caller's workspace (sift_sparse_prefill_ex)
   sift::PlanTables pt{};
   sift::WorkTables wt{};
   int32_t* counts = nullptr;   // [num_rows]
@@ -334,11 +335,18 @@ const char* sift_status_string(int32_t status) {
   }
 }
 
-sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
-                             int32_t num_kv_heads, int32_t head_dim, int32_t tile,
-                             sift_plan** plan_out) {
-  if (layout == nullptr || plan_out == nullptr) return SIFT_E_NULL;
-  *plan_out = nullptr;
+}  // extern "C"
+
+namespace {
+
+// The plan's device memory: with ws == nullptr a hipMalloc of its own, else
+// the caller's workspace ws of ws_bytes (tables uploaded on `stream`, which
+// is waited for).  With bytes_only != nullptr only the size is computed.
+sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t num_kv_heads,
+                        int32_t head_dim, int32_t tile, void* ws, size_t ws_bytes,
+                        hipStream_t stream, size_t* bytes_only, sift_plan** plan_out) {
+  if (layout == nullptr || (plan_out == nullptr && bytes_only == nullptr)) return SIFT_E_NULL;
+  if (plan_out != nullptr) *plan_out = nullptr;
   if (num_q_heads < 1 || num_kv_heads < 1 || num_q_heads % num_kv_heads != 0) return SIFT_E_SHAPE;
   if (head_dim != 64 && head_dim != 128) return SIFT_E_UNSUPPORTED;
   if (tile != 16 && tile != 32 && tile != 64 && tile != 128) return SIFT_E_UNSUPPORTED;
@@ -389,29 +397,47 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   const size_t o_part_ml = align(o_part_o + slot_rows * head_dim * 4);  // fp32 or bf16 output
   const size_t total = o_part_ml + std::max<int64_t>(slot_rows, 1) * 8;
 
+  if (bytes_only != nullptr) {
+    *bytes_only = total;
+    return SIFT_OK;
+  }
+  if (ws != nullptr) {
+    if (ws_bytes < total) return SIFT_E_CAPACITY;
+    if (reinterpret_cast<uintptr_t>(ws) % 256 != 0) return SIFT_E_UNSUPPORTED;
+  }
   sift_plan* plan = new (std::nothrow) sift_plan();
   if (plan == nullptr) return SIFT_E_HIP;
   if (hipGetDevice(&plan->device) != hipSuccess) {
     delete plan;
     return SIFT_E_HIP;
   }
-  if (hipMalloc(&plan->dev, total) != hipSuccess) {
+  auto fail = [plan]() {
+    if (plan->owns_dev && plan->dev != nullptr) (void)hipFree(plan->dev);
     delete plan;
     return SIFT_E_HIP;
-  }
+  };
   plan->dev_bytes = total;
-  if (!blob.empty() &&
-      hipMemcpy(plan->dev, blob.data(), blob.size(), hipMemcpyHostToDevice) != hipSuccess) {
-    (void)hipFree(plan->dev);
-    delete plan;
-    return SIFT_E_HIP;
-  }
-  // the schedule's bucket sizes start at zero; each schedule pass leaves them so
-  if (hipMemset(static_cast<uint8_t*>(plan->dev) + o_hist, 0, kHistBytes) !=
-      hipSuccess) {
-    (void)hipFree(plan->dev);
-    delete plan;
-    return SIFT_E_HIP;
+  if (ws == nullptr) {
+    if (hipMalloc(&plan->dev, total) != hipSuccess) return fail();
+    if (!blob.empty() &&
+        hipMemcpy(plan->dev, blob.data(), blob.size(), hipMemcpyHostToDevice) != hipSuccess)
+      return fail();
+    // the schedule's bucket sizes start at zero; each schedule pass leaves them so
+    if (hipMemset(static_cast<uint8_t*>(plan->dev) + o_hist, 0, kHistBytes) != hipSuccess)
+      return fail();
+  } else {
+    // the caller's workspace, in stream order: the upload waits for earlier
+    // work on the stream (which may still read the workspace), and the host
+    // copy of the tables must outlive it
+    plan->dev = ws;
+    plan->owns_dev = false;
+    if (!blob.empty() && hipMemcpyAsync(plan->dev, blob.data(), blob.size(),
+                                        hipMemcpyHostToDevice, stream) != hipSuccess)
+      return fail();
+    if (hipMemsetAsync(static_cast<uint8_t*>(plan->dev) + o_hist, 0, kHistBytes, stream) !=
+        hipSuccess)
+      return fail();
+    if (hipStreamSynchronize(stream) != hipSuccess) return fail();
   }
   auto P = [plan](size_t off) {
     return reinterpret_cast<int32_t*>(static_cast<uint8_t*>(plan->dev) + off);
@@ -473,10 +499,30 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
   return SIFT_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
+                             int32_t num_kv_heads, int32_t head_dim, int32_t tile,
+                             sift_plan** plan_out) {
+  if (plan_out == nullptr) return SIFT_E_NULL;
+  return create_plan(layout, num_q_heads, num_kv_heads, head_dim, tile, nullptr, 0, nullptr,
+                     nullptr, plan_out);
+}
+
+sift_status sift_workspace_bytes(const sift_layout* layout, int32_t num_q_heads,
+                                 int32_t num_kv_heads, int32_t head_dim, int32_t tile,
+                                 size_t* bytes) {
+  if (bytes == nullptr) return SIFT_E_NULL;
+  return create_plan(layout, num_q_heads, num_kv_heads, head_dim, tile, nullptr, 0, nullptr,
+                     bytes, nullptr);
+}
+
 sift_status sift_plan_destroy(sift_plan* plan) {
   if (plan == nullptr) return SIFT_OK;
   sift_status st = SIFT_OK;
-  if (plan->dev != nullptr) {
+  if (plan->dev != nullptr && plan->owns_dev) {
     if (hipDeviceSynchronize() != hipSuccess) st = SIFT_E_HIP;
     if (hipFree(plan->dev) != hipSuccess) st = SIFT_E_HIP;
   }
@@ -686,6 +732,42 @@ sift_status sift_sparse_prefill(const sift_tensor* q, const sift_tensor* k, cons
   if (st == SIFT_OK && hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess)
     st = SIFT_E_HIP;
   const sift_status st2 = sift_plan_destroy(plan);
+  return st != SIFT_OK ? st : st2;
+}
+
+sift_status sift_sparse_prefill_ex(const sift_tensor* q, const sift_tensor* k,
+                                   const sift_tensor* v, const sift_layout* doc_offsets,
+                                   const uint8_t* local_bitmap, const uint8_t* cross_bitmap,
+                                   int32_t tile, float softmax_scale, void* workspace,
+                                   size_t workspace_bytes, sift_tensor* out, void* stream) {
+  if (q == nullptr || k == nullptr || v == nullptr || out == nullptr || doc_offsets == nullptr)
+    return SIFT_E_NULL;
+  if (workspace == nullptr) return SIFT_E_NULL;
+  {
+    if (q->heads < 1 || k->heads < 1 || q->heads % k->heads != 0) return SIFT_E_SHAPE;
+    if (q->head_dim != 64 && q->head_dim != 128) return SIFT_E_UNSUPPORTED;
+    if (tile != 16 && tile != 32 && tile != 64 && tile != 128) return SIFT_E_UNSUPPORTED;
+    HostPlan hp;
+    sift_status st0 = build_host_plan(doc_offsets, q->heads, k->heads, tile, hp);
+    if (st0 != SIFT_OK) return st0;
+    st0 = check_io(q, k, v, out, hp.num_tokens, q->heads, k->heads, q->head_dim, tile);
+    if (st0 != SIFT_OK) return st0;
+    if (hp.la_bytes > 0 && local_bitmap == nullptr) return SIFT_E_NULL;
+    if (hp.ca_bytes > 0 && cross_bitmap == nullptr) return SIFT_E_NULL;
+    size_t need = 0;
+    st0 = create_plan(doc_offsets, q->heads, k->heads, q->head_dim, tile, nullptr, 0, nullptr,
+                      &need, nullptr);
+    if (st0 != SIFT_OK) return st0;
+    if (workspace_bytes < need) return SIFT_E_CAPACITY;
+    if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return SIFT_E_UNSUPPORTED;
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  sift_plan* plan = nullptr;
+  sift_status st = create_plan(doc_offsets, q->heads, k->heads, q->head_dim, tile, workspace,
+                               workspace_bytes, s, nullptr, &plan);
+  if (st != SIFT_OK) return st;
+  st = sift_plan_run(plan, q, k, v, local_bitmap, cross_bitmap, softmax_scale, out, stream);
+  const sift_status st2 = sift_plan_destroy(plan);  // host state only: the workspace is the caller's
   return st != SIFT_OK ? st : st2;
 }
 

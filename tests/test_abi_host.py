@@ -14,7 +14,7 @@ def test_library_loads_and_exports_every_declared_symbol():
     L = B.lib()
     names = B.header_functions()
     assert "sift_sparse_prefill" in names and "sift_decode_tiles" in names
-    assert len(names) == 14
+    assert len(names) == 16
     for n in names:
         assert hasattr(L, n), n
     # the binding declares every one of them too
@@ -107,3 +107,49 @@ def test_extract_sizes_and_argument_checks_on_the_host():
     assert call(q, k, la=0) == 1
     bad = np.array([0, 64, 64], dtype=np.int32)               # an empty document
     assert call(q, k, offs_p=bad.ctypes.data_as(ctypes.c_void_p)) == 3
+
+
+def _ws_bytes(so, ps, hq=4, hkv=2, d=128, tile=64):
+    lay, keep = B.layout_struct(so, ps)
+    n = ctypes.c_size_t()
+    st = B.lib().sift_workspace_bytes(ctypes.byref(lay), hq, hkv, d, tile, ctypes.byref(n))
+    return st, n.value
+
+
+def test_workspace_bytes_on_the_host():
+    so, ps = [0, 64, 128, 160], [0, 3]
+    st, n = _ws_bytes(so, ps)
+    assert st == 0 and n > 0 and n % 8 == 0
+    # more heads, more tokens or a smaller tile never need less
+    assert _ws_bytes(so, ps, hq=8, hkv=2)[1] > n
+    assert _ws_bytes([0, 640, 1280, 1600], ps)[1] > n
+    assert _ws_bytes(so, ps, tile=16)[1] > n
+    # the same checks as a plan: bad layouts, heads, tiles
+    assert _ws_bytes([0, 0, 128, 160], ps)[0] == 3
+    assert _ws_bytes(so, ps, hq=3)[0] == 2
+    assert _ws_bytes(so, ps, tile=48)[0] == 4
+    assert _ws_bytes(so, ps, d=96)[0] == 4
+
+
+def _prefill_ex(q, k, v, so, ps, ws, ws_bytes, tile=64, la=1, ca=1):
+    lay, keep = B.layout_struct(so, ps)
+    out = _t(q.tokens, q.heads, q.head_dim, q.dtype)
+    return B.lib().sift_sparse_prefill_ex(
+        ctypes.byref(q), ctypes.byref(k), ctypes.byref(v), ctypes.byref(lay), ctypes.c_void_p(la),
+        ctypes.c_void_p(ca), tile, ctypes.c_float(0.0), ctypes.c_void_p(ws), ws_bytes,
+        ctypes.byref(out), None)
+
+
+def test_prefill_ex_rejects_workspace_and_arguments_on_the_host():
+    """Every check happens before the device is touched: the fake device
+    pointers below are never dereferenced."""
+    so, ps = [0, 64, 128, 160], [0, 3]
+    q, k = _t(160, 4, 128), _t(160, 2, 128)
+    n = _ws_bytes(so, ps)[1]
+    assert _prefill_ex(q, k, k, so, ps, 0, n) == 1                       # no workspace
+    assert _prefill_ex(q, k, k, so, ps, 1 << 20, n - 1) == 5             # too small
+    assert _prefill_ex(q, k, k, so, ps, (1 << 20) + 64, n) == 4          # not 256-byte aligned
+    assert _prefill_ex(_t(161, 4, 128), k, k, so, ps, 1 << 20, n) == 2   # shapes
+    assert _prefill_ex(q, k, k, [0, 64, 32, 160], ps, 1 << 20, n) == 3   # layout
+    assert _prefill_ex(q, k, k, so, ps, 1 << 20, n, tile=48) == 4        # tile
+    assert _prefill_ex(q, k, k, so, ps, 1 << 20, n, la=0) == 1           # bit vectors
