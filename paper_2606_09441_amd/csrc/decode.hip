@@ -131,7 +131,9 @@ __global__ __launch_bounds__(1024) void decode_scan(const int32_t* __restrict__ 
 // that list them, and to the merged step list: at T >= 64 one or two steps
 // per tile (tile_steps); at T < 64 one step per group of G = 64 / T
 // consecutive tiles of a segment that any M-block lists (emit_grouped).
-template <int kNb>  // most M-blocks of a list unit (128 / T, at least 2)
+// kNb: most M-blocks of a list unit (128 / T, at least 2); kHalves: T = 128
+// (a tile is one or two 64-key steps).
+template <int kNb, bool kHalves>
 struct Emitter {
   int32_t* col;
   int2* steps;
@@ -159,6 +161,21 @@ struct Emitter {
 
   __device__ __forceinline__ void emit(unsigned listed, int32_t n) {
     lists(listed, n);
+    if constexpr (!kHalves) {
+      // T = 64: one step per listed tile, in lane order
+      const unsigned long long mu = __ballot(listed != 0u);
+      if (listed != 0u) {
+        const unsigned diag = (n >= m0 && n < m0 + nb) ? 1u << (n - m0) : 0u;
+        const int info = pt->tile_len[n] | static_cast<int>(listed << kStepListedShift) |
+                         static_cast<int>(diag << kStepDiagShift);
+        const int32_t idx = ps + __popcll(mu & below);
+        const int2 st = make_int2(kv_row0(*pt, pages, n), info);
+        steps[idx] = st;
+        if (whole && idx - base < kFirstSteps) wt->rec[w0].first[idx - base] = st;
+      }
+      ps += __popcll(mu);
+      return;
+    }
     // one or two steps per listed tile, in lane order
     const TileSteps ts = tile_steps(*pt, pages, n, listed, m0, nb);
     const unsigned long long mu1 = __ballot(ts.cnt >= 1), mu2 = __ballot(ts.cnt >= 2);
@@ -220,9 +237,9 @@ struct Emitter {
 };
 
 // kNb: the most M-blocks of a list unit (2 at T >= 64, 4 at T = 32, 8 at
-// T = 16); kGrouped: T < 64 (steps are groups of tiles).  Separate
-// instances keep the T >= 64 one free of the wider unit's registers.
-template <int kNb, bool kGrouped>
+// T = 16); kGrouped: T < 64 (steps are groups of tiles); kHalves: T = 128.
+// Separate instances keep the T = 64 one free of the other sizes' work.
+template <int kNb, bool kGrouped, bool kHalves>
 __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt,
                                                     const uint8_t* __restrict__ la,
                                                     const uint8_t* __restrict__ ca,
@@ -236,7 +253,7 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   const int nb = wt.lu_nb[u];
   const unsigned all = (1u << nb) - 1u;
   const int64_t r0 = static_cast<int64_t>(h) * pt.num_tiles + m0;
-  Emitter<kNb> e;
+  Emitter<kNb, kHalves> e;
   e.col = col;
   e.steps = wt.steps;
   e.pt = &pt;
@@ -518,13 +535,16 @@ hipError_t launch_decode(const PlanTables& pt, const WorkTables& wt, const uint8
   if (wt.num_units == 0) return hipSuccess;
   const dim3 wgrid(static_cast<unsigned>((wt.num_units + 3) / 4));
   if (pt.group == 4)
-    hipLaunchKernelGGL((decode_write<8, true>), wgrid, dim3(256), 0, stream, pt, wt, la, ca, row_ptr,
-                       col_idx, pages);
+    hipLaunchKernelGGL((decode_write<8, true, false>), wgrid, dim3(256), 0, stream, pt, wt, la, ca,
+                       row_ptr, col_idx, pages);
   else if (pt.group == 2)
-    hipLaunchKernelGGL((decode_write<4, true>), wgrid, dim3(256), 0, stream, pt, wt, la, ca, row_ptr,
-                       col_idx, pages);
+    hipLaunchKernelGGL((decode_write<4, true, false>), wgrid, dim3(256), 0, stream, pt, wt, la, ca,
+                       row_ptr, col_idx, pages);
+  else if (pt.halves == 2)
+    hipLaunchKernelGGL((decode_write<2, false, true>), wgrid, dim3(256), 0, stream, pt, wt, la, ca,
+                       row_ptr, col_idx, pages);
   else
-    hipLaunchKernelGGL((decode_write<2, false>), wgrid, dim3(256), 0, stream, pt, wt, la, ca,
+    hipLaunchKernelGGL((decode_write<2, false, false>), wgrid, dim3(256), 0, stream, pt, wt, la, ca,
                        row_ptr, col_idx, pages);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
