@@ -36,15 +36,20 @@
 //    wait for it before every LDS read.
 //  * Software pipeline, one barrier per step.  During step t a wavefront
 //    computes S(t+1) = K(t+1) Q^T on the MFMA pipe while the VALU turns S(t)
-//    into P(t) (exp2, bf16 rounding, row sum), then O += V(t)^T P(t) on the
-//    MFMA pipe while the VALU reduces the row max of S(t+1).  Meanwhile the
-//    DMA brings K(t+2) and V(t+1): K runs one tile ahead of V, each with two
-//    LDS slots (a slot is refilled only after the barrier that follows its
-//    last read).  Two workgroups per CU (2 wavefronts per SIMD) cover the
-//    remaining stalls.
-//  * Online softmax in the log2 domain with a lazy reference max (rescale
-//    only when a tile's max exceeds it by more than kLazy); P is rounded to
-//    bf16 and the row sum adds exactly those rounded values
+//    into P(t) (exp2, bf16 rounding, row sum), then O += V(t)^T P(t).
+//    Meanwhile the DMA brings K(t+2) and V(t+1): K runs one tile ahead of
+//    V, each with two LDS slots (a slot is refilled only after the barrier
+//    that follows its last read).  Two workgroups per CU (2 wavefronts per
+//    SIMD) cover the remaining stalls.
+//  * Online softmax in the log2 domain, in two launches.  On gfx950 plain
+//    VALU work does not overlap the MFMAs (the exponentials do), so every
+//    VALU instruction per step counts.  The first launch takes no row max
+//    per tile: a row's reference is the max of the first tile it sees, and
+//    later tiles' weights are checked by their sums (kSumMax).  If a check
+//    fails anywhere, or an output comes out non-finite, the launch raises a
+//    flag and the second launch does every unit again with a lazy running
+//    max (kLazy); otherwise the second launch returns at once.  P is rounded
+//    to bf16 and the row sum adds exactly those rounded values
 //    (v_dot2_f32_bf16 against 1.0), so normalisation matches the weights
 //    the MFMA used.
 //  * Workgroup -> unit mapping comes from the plan's schedule: units are
@@ -82,6 +87,24 @@ constexpr int kBufferWord3 = 0x00020000;  // gfx9-family raw buffer resource wor
 // when a tile's max exceeds it by more than kLazy.  exp2 arguments stay
 // <= kLazy, so P <= 2^kLazy: no overflow, and the same bf16 relative precision.
 constexpr float kLazy = 8.0f;
+
+// The pass over all units does not take a tile's row max at all.  A row's
+// reference max is the max of the first tile that gives it a key; later
+// tiles' weights P = 2^(s c - mref) are formed against it and bounded by
+// their sums: while a lane's share of a tile's sum (32 weights) is <=
+// kSumMax, every P is finite and <= kSumMax (bf16 P keeps its relative
+// precision at any magnitude, and l stays below 2^80).  When some share
+// exceeds it (a score more than 55 log2 units above the reference, or an
+// exp2 overflow), or O or l ends up infinite or NaN (|v| beyond about 2^50
+// with such weights, or non-finite inputs), the launch is flagged and a
+// second launch does every unit again with the lazy reference above
+// (kLazy), whose weights are <= 2^kLazy.  Neither happens with scores of
+// the usual range.
+constexpr float kSumMax = 0x1p60f;
+
+// Workgroups of the launch that does the units again (it returns at once
+// when the first launch raised no flag).
+constexpr int kRedoGrid = 512;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 x) { return __builtin_bit_cast(bf16x8, x); }
 
@@ -294,15 +317,16 @@ __device__ __forceinline__ float tile_max(const f32x16& s0, const f32x16& s1) {
   return swap_max(fmaxf(m0, m1));
 }
 
-// Lazy rescale: move the reference max (and rescale O and l) only when the
-// tile's scaled max mxs exceeds it by more than kLazy.
+// Move the reference max (and rescale O and l) when the tile's scaled max
+// mxs exceeds it by more than kMargin: kLazy in the exact pass; 0 when a
+// row takes its first reference.
 // kG > 1: rows of one wavefront see different sub-tiles, so a lane can
 // still hold mref = -inf (no key yet) when another grows: its factor is 1,
 // not 2^(-inf - -inf).  At T >= 64 every row of a wavefront sees the same
 // tiles and has a key from its first step on.
-template <int kG = 1>
+template <int kG = 1, bool kLazyRule = true>
 __device__ __forceinline__ void rescale(RowState& st, float mxs) {
-  const bool grow = mxs > st.mref + kLazy;
+  const bool grow = kLazyRule ? mxs > st.mref + kLazy : mxs > st.mref;
   if (__builtin_amdgcn_ballot_w64(grow)) {
     const float mnew = grow ? mxs : st.mref;
     float alpha = __builtin_amdgcn_exp2f(st.mref - mnew);
@@ -344,6 +368,15 @@ __device__ __forceinline__ void softmax_exp(const f32x16& s0, const f32x16& s1, 
   lsum += psum;
 }
 
+// Rows without a reference take the row max of the next tile (scores s0,
+// s1) before its weights are formed.
+template <int kG>
+__device__ __forceinline__ void first_ref(RowState& rs, const f32x16& s0, const f32x16& s1,
+                                          float c) {
+  if (__builtin_amdgcn_ballot_w64(rs.mref == -INFINITY))
+    rescale<kG, false>(rs, tile_max(s0, s1) * c);
+}
+
 __device__ __forceinline__ void pv_tile(const PvArgs& v, int slot_off, const bf16x8 (&pb)[4],
                                         RowState& st) {
 #pragma unroll
@@ -375,6 +408,16 @@ __device__ __forceinline__ void interleave_pv_max() {
   }
 }
 
+// PV with nothing to interleave: the transpose reads kept ahead.
+__device__ __forceinline__ void pace_pv() {
+  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if (i < 14) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  }
+}
+
 // The same with nothing to interleave: keep the fragment reads two MFMAs
 // ahead (an unconstrained schedule issues all of them first and runs out of
 // registers).
@@ -387,7 +430,12 @@ __device__ __forceinline__ void pace_qk() {
   }
 }
 
-template <bool kOutF32, int kG>
+// kRedo = false: the first pass; workgroup b takes the unit of launch slot
+// b and flags the launch (wt.redo[0]) if a weight check fails.  kRedo =
+// true: the exact pass; when the flag is set, kRedoGrid workgroups do every
+// unit again, then the last one to finish clears the flag for the next
+// launch; otherwise they return at once.
+template <bool kOutF32, int kG, bool kRedo>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTables wt,
                                                            AttnArgs a) {
   // K slot 0, K slot 1, V slot 0, V slot 1 (16 KB each)
@@ -397,248 +445,26 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTa
   // same value and reads back its own write)
   __shared__ int slot_park;
 
-  // the work unit's record, loaded whole before anything else
-  const int4* __restrict__ rp = reinterpret_cast<const int4*>(wt.launch + blockIdx.x);
-  const int4 ra = rp[0];  // head, kv head, blocks, slot
-  const int4 rb = rp[1];  // first token and length of the two M-blocks
-  const int4 rc = rp[2];  // step offset, step count, step 0
-  const int4 rd = rp[3];  // steps 1, 2
-  const int h = ra.x;
-  const int kvh = ra.y;
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
-  const int l32 = lane & 31;
-  const int hf = lane >> 5;
-  const int hq = a.hq;
-  const int hkv = a.hkv;
-  const int kstride = hkv * kD;
-  const int row_bytes = kstride * 2;
-  const int qrow = (wave & 1) * 32 + l32;  // query row inside this wavefront's M-block
-  slot_park = ra.w;
-  const float c = a.scale_log2;
-  const __bf16* __restrict__ qp = static_cast<const __bf16*>(a.q);
-  const __bf16* __restrict__ kp = static_cast<const __bf16*>(a.k);
-  const __bf16* __restrict__ vp = static_cast<const __bf16*>(a.v);
-  lds_bf16* lds = (lds_bf16*)smem;
-  // LDS byte addresses of this wavefront's first DMA row in each slot
-  const int lds0 = static_cast<int>(reinterpret_cast<size_t>(lds)) + 16 * wave * kD * 2;
-  const int kdst[2] = {lds0, lds0 + 2 * kTile};
-  const int vdst[2] = {lds0 + 4 * kTile, lds0 + 6 * kTile};
-
-  // global byte offsets of the DMA rows 16w + 4it + l/16, logical chunk
-  // (l%16) ^ swizzle(row), which lands at physical chunk l%16 of that row.
-  // K: swizzle = row & 15 = 4it + l/16, so the chunk for it is the chunk for
-  // it = 0 XOR 4it.  V: swizzle = 4(row & 3) = 4(l/16), the same for every it.
-  int koff0, voff0;
-  {
-    const int rsub = lane >> 4;
-    const int pc = lane & 15;
-    const int row = 16 * wave + rsub;
-    koff0 = row * row_bytes + ((pc ^ rsub) * 16);
-    voff0 = row * row_bytes + ((pc ^ (4 * rsub)) * 16);
-  }
-  const int rstep = 4 * row_bytes;
-
-  // Q^T fragments (B operand of S^T = K Q^T): lane holds query row qrow,
-  // dims 16s + 8hf .. +7 for k-step s.
-  // wavefronts 0, 1 take M-block m0, wavefronts 2, 3 M-block m0 + 1 (a
-  // missing block has no rows)
-  const int qtok0 = wave < 2 ? rb.x : rb.y;
-  const int qlen = wave < 2 ? rb.z : rb.w;
-  bf16x8 qf[8];
-  {
-    const bool live = qrow < qlen;
-    const __bf16* src = qp + (static_cast<int64_t>(qtok0 + qrow) * hq + h) * kD + 8 * hf;
-#pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      u32x4 x = u32x4{0u, 0u, 0u, 0u};
-      if (live) x = *reinterpret_cast<const u32x4*>(src + 16 * s);
-      qf[s] = as_bf16x8(x);
-    }
-  }
-
-  // the unit's merged steps
-  const int2* __restrict__ steps = wt.steps + rc.x;
-  const uint32_t* __restrict__ subs = wt.sub + rc.x;  // read only when kG > 1
-  const int nsteps = rc.y;
-  const int64_t kv_head_off = static_cast<int64_t>(kvh) * kD;
-  auto rsrc = [&](const __bf16* base, const Step& s) {
-    return tile_rsrc(base + static_cast<int64_t>(s.tok0) * kstride + kv_head_off, s.len(),
-                     row_bytes);
-  };
-  auto fetch = [&](int i) { return steps[i < nsteps ? i : 0]; };
-
-  RowState rs;
-#pragma unroll
-  for (int db = 0; db < 4; ++db)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) rs.o[db][v] = 0.f;
-  rs.mref = -INFINITY;
-  rs.lsum = 0.f;
-
-  const int lds_base = static_cast<int>(reinterpret_cast<size_t>(lds));
-  QkArgs qa;
-  qa.addr = lds_base + l32 * kD * 2 + 32 * ((l32 & 15) >> 1) + 16 * (hf ^ (l32 & 1));
-  PvArgs pva;
-  {
-    const int cbase = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-    const int z = (lane & 15) >> 2;
-    pva.addr = lds_base + 4 * kTile + (z + 4 * hf) * kD * 2 + 64 * z + 16 * (cbase >> 3) +
-               2 * (cbase & 7);
-  }
-
-  // an empty list leaves O = 0 and l = 0: the epilogue writes zeros
-  if (nsteps > 0) {
-    // ---- prologue: K(0), V(0), K(1) into LDS; S(0) = K(0) Q^T
-    Step c0 = make_step(make_int2(rc.z, rc.w), true);
-    // steps past the count carry stale values: make_step marks them invalid
-    Step c1 = make_step(make_int2(rd.x, rd.y), nsteps > 1);
-    Step c2 = make_step(make_int2(rd.z, rd.w), nsteps > 2);
-    if constexpr (kG > 1) {
-      c0.sub = __builtin_amdgcn_readfirstlane(subs[0]);
-      c1.sub = __builtin_amdgcn_readfirstlane(subs[nsteps > 1 ? 1 : 0]);
-      c2.sub = __builtin_amdgcn_readfirstlane(subs[nsteps > 2 ? 2 : 0]);
-    }
-    dma_tile<true>(kdst[0], koff0, rstep, rsrc(kp, c0));
-    dma_tile<false>(vdst[0], voff0, rstep, rsrc(vp, c0));
-    dma_tile<true>(kdst[1], koff0, rstep, rsrc(kp, c1.valid ? c1 : c0));
-    wait_dma();
-    __syncthreads();
-    f32x16 sa0, sa1, sb0, sb1;  // score tiles of even / odd steps
-    if (c0.in(wave)) {
-      qk_tile(qa, 0, qf, sa0, sa1);
-      pace_qk();
-      if (needs_mask(c0, wave) || sub_partial<kG>(c0, wave)) {
-        mask_tile(sa0, sa1, c0, wave, qrow, hf);
-        mask_sub<kG>(sa0, sa1, c0, wave, l32);
-      }
-      rescale<kG>(rs, tile_max(sa0, sa1) * c);
-    }
-    __syncthreads();  // K slot 0 is refilled by step 0
-
-    // ---- step t: S(t) is in (cur0, cur1); computes S(t+1) into (nx0, nx1)
-    auto step = [&](int t, const int par, f32x16& cur0, f32x16& cur1, f32x16& nx0,
-                    f32x16& nx1) {
-      // V(t+1) and K(t+2) (past the end of the list: step t's tiles again,
-      // into slots nobody reads, so the DMA stays unconditional)
-      dma_tile<false>(vdst[par ^ 1], voff0, rstep, rsrc(vp, c1.valid ? c1 : c0));
-      dma_tile<true>(kdst[par], koff0, rstep, rsrc(kp, c2.valid ? c2 : c0));
-      const int2 raw3 = fetch(t + 3);  // decoded after the DMA wait below
-      unsigned sub3 = 0u;
-      if constexpr (kG > 1) sub3 = subs[t + 3 < nsteps ? t + 3 : 0];
-      const bool a0 = c0.in(wave);
-      const bool a1 = c1.valid && c1.in(wave);
-      // keep the per-read addresses derived inside the step (hoisted out of
-      // the loop they would each hold a register)
-      asm volatile("" : "+v"(qa.addr), "+v"(pva.addr), "+v"(koff0), "+v"(voff0));
-      const int kso = (par ^ 1) * 2 * kTile;  // byte offset of K slot par ^ 1
-      const int vso = par * 2 * kTile;        // byte offset of V slot par
-      // one straight-line body per case.  When this wavefront's M-block lists
-      // tile t but not tile t+1 (or t is the last step), the full body runs
-      // and S(t+1) is masked out entirely: K(t+1) is only read, never
-      // weighted.  Without tile t, the body leaves out P(t) and V(t).
-      auto body = [&](auto A0, auto A1) {
-        constexpr bool kA0 = decltype(A0)::value, kA1 = decltype(A1)::value;
-        // distinct addresses per body: reads common to two bodies would be
-        // hoisted above the branch, all live at once
-        asm volatile("" : "+v"(qa.addr), "+v"(pva.addr));
-        bf16x8 pb[4];
-        if constexpr (kA1) {
-          qk_tile(qa, kso, qf, nx0, nx1);
-        } else {
-#pragma unroll
-          for (int v = 0; v < 16; ++v) nx0[v] = nx1[v] = -INFINITY;
-        }
-        if constexpr (kA0) softmax_exp(cur0, cur1, c, exp_base(rs), pb, rs.lsum);
-        if constexpr (kA0 && kA1) {
-          interleave_qk_exp();
-          // P(t) and l are complete here: otherwise the exponentials sink
-          // past the mask branch, away from the MFMAs they overlap
-          asm volatile("" : "+v"(pb[0]), "+v"(pb[1]), "+v"(pb[2]), "+v"(pb[3]), "+v"(rs.lsum));
-        }
-        if constexpr (!kA0 && kA1) pace_qk();
-        if constexpr (kA1) {
-          if (!a1 || needs_mask(c1, wave) || sub_partial<kG>(c1, wave)) {
-            mask_tile(nx0, nx1, c1, wave, qrow, hf, !a1);
-            mask_sub<kG>(nx0, nx1, c1, wave, l32);
-          }
-        }
-        float mx = -INFINITY;
-        if constexpr (kA0) pv_tile(pva, vso, pb, rs);
-        if constexpr (kA1) mx = tile_max(nx0, nx1);
-        if constexpr (kA0 && kA1) interleave_pv_max();
-        if constexpr (kA1) rescale<kG>(rs, mx * c);
+  if constexpr (!kRedo) {
+    const int4* __restrict__ rp = reinterpret_cast<const int4*>(wt.launch + blockIdx.x);
+#include "attn_bf16_unit.inc"
+  } else {
+    if (__hip_atomic_load(&wt.redo[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) return;
+    for (int u = blockIdx.x; u < wt.grid; u += gridDim.x) {
+      auto unit = [&](const int4* __restrict__ rp) {
+#include "attn_bf16_unit.inc"
       };
-      using T = std::true_type;
-      using F = std::false_type;
-      if (a0)
-        body(T{}, T{});
-      else if (a1)
-        body(F{}, T{});
-      else
-        body(F{}, F{});
-      wait_dma();
-      __syncthreads();
-      c0 = c1;
-      c1 = c2;
-      c2 = make_step(raw3, t + 3 < nsteps);
-      if constexpr (kG > 1) c2.sub = __builtin_amdgcn_readfirstlane(sub3);
-    };
-
-    for (int t = 0; t < nsteps; t += 2) {
-      step(t, 0, sa0, sa1, sb0, sb1);
-      if (t + 1 >= nsteps) break;
-      step(t + 1, 1, sb0, sb1, sa0, sa1);
+      unit(reinterpret_cast<const int4*>(wt.launch + u));
+      __syncthreads();  // LDS (slots, slot_park) is reused by the next unit
     }
-  }
-
-  // The lane index is taken afresh (mbcnt of an opaque zero) so that no
-  // per-lane index stays in a register across the main loop.
-  unsigned zero;
-  asm volatile("s_mov_b32 %0, 0" : "=s"(zero));
-  const int ln = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, zero));
-  const int row = (wave & 1) * 32 + (ln & 31);  // = qrow
-  const int half = ln >> 5;                     // = hf
-  if (row >= qlen) return;
-  const float lt = swap_sum(rs.lsum);
-
-  const float inv = lt > 0.f ? 1.f / lt : 0.f;
-
-  // ---- lane writes O = O^T / l, dims 32db + 8i + 4hf .. +3 of its row, in
-  // the output's type.  A piece of a split unit writes to its slot instead
-  // (plus the row's reference max and sum, for the merge).  A unit's query
-  // rows are at most kUnitRows consecutive tokens (blocks m0, m0 + 1 are
-  // adjacent in the packed order), so token t goes to row t mod kUnitRows of
-  // the slot.  Both cases share one store sequence.
-  const int slot = __builtin_amdgcn_readfirstlane(slot_park);
-  const int tok = qtok0 + row;
-  void* obuf = a.out;
-  int64_t obase = (static_cast<int64_t>(tok) * hq + h) * kD + 4 * half;
-  if (slot >= 0) {
-    const int64_t slot_row = static_cast<int64_t>(slot) * kUnitRows + (tok & (kUnitRows - 1));
-    obuf = wt.part_o;
-    obase = slot_row * kD + 4 * half;
-    if (half == 0) wt.part_ml[slot_row] = make_float2(rs.mref, lt);
-  }
-#pragma unroll
-  for (int db = 0; db < 4; ++db)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int d = 32 * db + 8 * i;
-      f32x4 x = f32x4{rs.o[db][4 * i] * inv, rs.o[db][4 * i + 1] * inv,
-                      rs.o[db][4 * i + 2] * inv, rs.o[db][4 * i + 3] * inv};
-      if constexpr (kOutF32) {
-        *reinterpret_cast<f32x4*>(static_cast<float*>(obuf) + obase + d) = x;
-      } else {
-        const bf16x2 y0 = bf16x2{static_cast<__bf16>(x[0]), static_cast<__bf16>(x[1])};
-        const bf16x2 y1 = bf16x2{static_cast<__bf16>(x[2]), static_cast<__bf16>(x[3])};
-        u32x2 w;
-        w[0] = __builtin_bit_cast(unsigned, y0);
-        w[1] = __builtin_bit_cast(unsigned, y1);
-        *reinterpret_cast<u32x2*>(static_cast<__bf16*>(obuf) + obase + d) = w;
+    if (threadIdx.x == 0) {
+      __threadfence();
+      if (atomicAdd(&wt.redo[1], 1) == static_cast<int>(gridDim.x) - 1) {
+        atomicExch(&wt.redo[0], 0);
+        atomicExch(&wt.redo[1], 0);
       }
     }
+  }
 }
 
 // Merge the pieces of the split units.  Piece p left its normalised
@@ -729,25 +555,29 @@ hipError_t launch_attn_bf16(const PlanTables& pt, const WorkTables& wt, const At
     return hipErrorInvalidValue;
   if (wt.grid == 0) return hipSuccess;
   const int g = a.tile < kT ? kT / a.tile : 1;  // key tiles per 64-key step
-  if (a.out_f32) {
-    if (g == 4)
-      hipLaunchKernelGGL((attn_bf16_kernel<true, 4>), dim3(wt.grid), dim3(256), 0, stream, pt, wt, a);
-    else if (g == 2)
-      hipLaunchKernelGGL((attn_bf16_kernel<true, 2>), dim3(wt.grid), dim3(256), 0, stream, pt, wt, a);
-    else
-      hipLaunchKernelGGL((attn_bf16_kernel<true, 1>), dim3(wt.grid), dim3(256), 0, stream, pt, wt, a);
-  } else {
-    if (g == 4)
-      hipLaunchKernelGGL((attn_bf16_kernel<false, 4>), dim3(wt.grid), dim3(256), 0, stream, pt, wt,
-                         a);
-    else if (g == 2)
-      hipLaunchKernelGGL((attn_bf16_kernel<false, 2>), dim3(wt.grid), dim3(256), 0, stream, pt, wt,
-                         a);
-    else
-      hipLaunchKernelGGL((attn_bf16_kernel<false, 1>), dim3(wt.grid), dim3(256), 0, stream, pt, wt,
-                         a);
-  }
-  hipError_t e = hipGetLastError();
+  // the first pass over every unit, then the exact pass (which returns at
+  // once unless the first raised its flag)
+  auto launch = [&](auto out_f32, auto group) {
+    constexpr bool kF = decltype(out_f32)::value;
+    constexpr int kGr = decltype(group)::value;
+    hipLaunchKernelGGL((attn_bf16_kernel<kF, kGr, false>), dim3(wt.grid), dim3(256), 0, stream, pt,
+                       wt, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((attn_bf16_kernel<kF, kGr, true>), dim3(kRedoGrid), dim3(256), 0, stream,
+                       pt, wt, a);
+    return hipGetLastError();
+  };
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I4 = std::integral_constant<int, 4>;
+  hipError_t e;
+  if (a.out_f32)
+    e = g == 4 ? launch(std::true_type{}, I4{})
+               : g == 2 ? launch(std::true_type{}, I2{}) : launch(std::true_type{}, I1{});
+  else
+    e = g == 4 ? launch(std::false_type{}, I4{})
+               : g == 2 ? launch(std::false_type{}, I2{}) : launch(std::false_type{}, I1{});
   if (e != hipSuccess || wt.num_splits == 0) return e;
   if (a.out_f32)
     hipLaunchKernelGGL(combine_kernel<true>, dim3(wt.num_splits, kUnitRows / 32), dim3(256), 0,

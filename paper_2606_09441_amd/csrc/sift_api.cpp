@@ -391,7 +391,9 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   const size_t o_sub = align(o_steps + (std::max<int64_t>(step_cap, 1) + 8) * 8);
   // per-step sub-tile masks, T < 64 only
   const size_t o_hist = align(o_sub + (tile < 64 ? (std::max<int64_t>(step_cap, 1) + 8) * 4 : 0));
-  constexpr size_t kHistBytes = sift::kNumXcd * sift::kSchedBuckets * 4;
+  // the schedule's bucket sizes, then the bf16 attention's redo flag and
+  // counter: zero at creation, and left so by every pass that uses them
+  constexpr size_t kHistBytes = sift::kNumXcd * sift::kSchedBuckets * 4 + 2 * 4;
   const size_t o_part_o = align(o_hist + kHistBytes);
   const int64_t slot_rows = hp.part_slots * sift::kUnitRows;
   const size_t o_part_ml = align(o_part_o + slot_rows * head_dim * 4);  // fp32 or bf16 output
@@ -472,6 +474,7 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   plan->wt.splits = reinterpret_cast<const int4*>(P(o_splits));
   plan->wt.part_o = static_cast<void*>(P(o_part_o));
   plan->wt.part_ml = reinterpret_cast<float2*>(P(o_part_ml));
+  plan->wt.redo = P(o_hist) + sift::kNumXcd * sift::kSchedBuckets;
   plan->wt.num_units = static_cast<int32_t>(U);
   plan->wt.num_work = static_cast<int32_t>(W);
   plan->wt.num_splits = static_cast<int32_t>(hp.splits.size() / 4);

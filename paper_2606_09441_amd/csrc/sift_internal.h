@@ -128,6 +128,9 @@ struct WorkTables {
   const int4* splits;         // [NS] {record of the first piece, first slot, slots, 0}
   void* part_o;               // [slots][kUnitRows][head_dim], output type (device scratch)
   float2* part_ml;            // [slots][kUnitRows] {reference max, row sum}
+  int32_t* redo;              // [2] bf16 attention: {flag: do every unit again exactly,
+                              // finished workgroups of that pass} (device scratch, zero
+                              // between launches)
   int32_t num_units;          // U
   int32_t num_work;           // W
   int32_t num_splits;         // NS

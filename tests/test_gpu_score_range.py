@@ -76,3 +76,49 @@ def test_falling_and_flat_scores():
     _parity(wl, "falling scores")
     wl.k = np.zeros_like(wl.k)
     _parity(wl, "flat scores")
+
+
+def test_redo_flag_is_cleared_for_the_next_launch():
+    """A launch that needs the exact pass, then launches that do not, on one
+    plan: each matches the oracle (a flag left set would only cost time; a
+    flag lost would leave the first launch wrong)."""
+    import torch
+    from gpu_helpers import DevWorkload
+    wl = W.custom(RAGGED, tile=64, hq=4, hkv=2, d=128, dtype="bf16", seed=8, p_la=0.5, p_ca=0.4)
+    k_plain = wl.k.copy()
+    rising = _rising(W.custom(RAGGED, tile=64, hq=4, hkv=2, d=128, dtype="bf16", seed=8,
+                              p_la=0.5, p_ca=0.4), 80.0)
+    lay = oracle_layout(wl)
+    dw = DevWorkload(wl)
+    try:
+        for name, kk in (("rising", rising.k), ("plain", k_plain), ("plain again", k_plain)):
+            dw.k.copy_(torch.from_numpy(kk).to(dw.k.device).to(dw.k.dtype))
+            out = dw.run().float().cpu().numpy()
+            ref = O.attention(lay, wl.q, kk, wl.v, wl.la, wl.ca)
+            err = max_abs(out, ref)
+            say(f"[range] one plan, {name} K: max-abs {err:.3e}")
+            assert np.isfinite(out).all() and err <= BF16_TOL, name
+    finally:
+        dw.close()
+
+
+def test_huge_values_with_rising_scores():
+    """V near 2^100 with scores rising along the segment by about 2^40
+    (weights within the first pass's bound): those weights times V overflow
+    fp32 in O, which the kernel notices and redoes exactly.  Compared
+    relative to the scale."""
+    big = 2.0 ** 100
+    wl = _rising(W.custom(RAGGED, tile=64, hq=4, hkv=2, d=128, dtype="bf16", seed=12,
+                          p_la=0.5, p_ca=0.4), 10.0)
+    wl.v = W.bf16_round((wl.v * big).astype(np.float32))
+    from gpu_helpers import DevWorkload
+    dw = DevWorkload(wl)
+    try:
+        out = dw.run(out_dtype=None).float().cpu().numpy()
+    finally:
+        dw.close()
+    ref = O.attention(oracle_layout(wl), wl.q, wl.k, wl.v, wl.la, wl.ca)
+    err = max_abs(out / big, ref / big)
+    say(f"[range] V ~ 2^100, K x1..10: max-abs / 2^100 {err:.3e}")
+    assert np.isfinite(out).all()
+    assert err <= BF16_TOL
