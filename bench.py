@@ -33,19 +33,29 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def attn_source_digest(csrc):
+    """sha256 over the attention kernel's source: attn_bf16.hip, then the
+    unit body it includes."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in ("attn_bf16.hip", "attn_bf16_unit.inc"):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
 def measured_traffic():
     """HBM bytes per attention launch from the committed rocprofv3 counter
     summary (FETCH_SIZE and WRITE_SIZE, scaled by the copy-kernel factors), or
     None when the attention kernel source has changed since it was taken."""
-    import hashlib
     import re
     path = os.path.join(ROOT, "profiles", "attn_bf16_long64k_hbm_traffic.md")
-    src = os.path.join(ROOT, "paper_2606_09441_amd", "csrc", "attn_bf16.hip")
+    csrc = os.path.join(ROOT, "paper_2606_09441_amd", "csrc")
     try:
         text = open(path).read()
         m = re.search(r"```json\s*(\{.*?\})\s*```", text, re.S)
         info = json.loads(m.group(1))
-        digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        digest = attn_source_digest(csrc)
     except (OSError, AttributeError, ValueError):
         return None
     return info["hbm_bytes_per_launch"] if info.get("source_sha256") == digest else None
