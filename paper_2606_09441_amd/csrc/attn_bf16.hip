@@ -430,14 +430,25 @@ __device__ __forceinline__ void pace_qk() {
   }
 }
 
+// The attention kernel's arguments as one aggregate, so that their place in
+// the kernel argument segment is fixed (the epilogue reads some of them from
+// there again).
+struct KernArgs {
+  PlanTables pt;
+  WorkTables wt;
+  AttnArgs a;
+};
+
 // kRedo = false: the first pass; workgroup b takes the unit of launch slot
 // b and flags the launch (wt.redo[0]) if a weight check fails.  kRedo =
 // true: the exact pass; when the flag is set, kRedoGrid workgroups do every
 // unit again, then the last one to finish clears the flag for the next
 // launch; otherwise they return at once.
 template <bool kOutF32, int kG, bool kRedo>
-__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(PlanTables pt, WorkTables wt,
-                                                           AttnArgs a) {
+__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(KernArgs ka) {
+  const PlanTables& pt = ka.pt;
+  const WorkTables& wt = ka.wt;
+  const AttnArgs& a = ka.a;
   // K slot 0, K slot 1, V slot 0, V slot 1 (16 KB each)
   __shared__ __attribute__((aligned(1024))) __bf16 smem[4 * kTile];
   // the unit's partial-result slot, parked in LDS for the epilogue so that
@@ -560,12 +571,12 @@ hipError_t launch_attn_bf16(const PlanTables& pt, const WorkTables& wt, const At
   auto launch = [&](auto out_f32, auto group) {
     constexpr bool kF = decltype(out_f32)::value;
     constexpr int kGr = decltype(group)::value;
-    hipLaunchKernelGGL((attn_bf16_kernel<kF, kGr, false>), dim3(wt.grid), dim3(256), 0, stream, pt,
-                       wt, a);
+    const KernArgs ka{pt, wt, a};
+    hipLaunchKernelGGL((attn_bf16_kernel<kF, kGr, false>), dim3(wt.grid), dim3(256), 0, stream, ka);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((attn_bf16_kernel<kF, kGr, true>), dim3(kRedoGrid), dim3(256), 0, stream,
-                       pt, wt, a);
+                       ka);
     return hipGetLastError();
   };
   using I1 = std::integral_constant<int, 1>;
