@@ -68,7 +68,7 @@ typedef enum sift_status {
   SIFT_E_NULL = 1,        /* a required pointer is NULL                       */
   SIFT_E_SHAPE = 2,       /* tensor shapes disagree (with each other/layout)  */
   SIFT_E_LAYOUT = 3,      /* malformed layout                                 */
-  SIFT_E_UNSUPPORTED = 4, /* valid, but outside this build (tile, D, dtype)   */
+  SIFT_E_UNSUPPORTED = 4, /* valid, but not implemented (tile, D, dtype)      */
   SIFT_E_CAPACITY = 5,    /* a caller buffer is too small                     */
   SIFT_E_HIP = 6,         /* a HIP runtime call failed                        */
   SIFT_E_PLAN = 7         /* the plan does not match the arguments            */
