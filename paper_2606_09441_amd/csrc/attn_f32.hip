@@ -31,6 +31,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(PlanTables pt, AttnArgs a
   __shared__ float Qs[T * D];
   __shared__ float Ks[T * KP];
   __shared__ float Vs[T * D];
+  __shared__ __attribute__((aligned(16))) float Ps[4][T];  // a wavefront's weights of one row
 
   const int64_t M = pt.num_tiles;
   const int64_t row = blockIdx.x;
@@ -79,6 +80,9 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(PlanTables pt, AttnArgs a
     __syncthreads();
 #pragma unroll
     for (int rr = 0; rr < R; ++rr) {
+      // rows one after another: interleaved by the scheduler, the unrolled
+      // rows' reads would all be held in registers at once
+      asm volatile("" ::: "memory");
       const int qr = w + 4 * rr;  // query row inside the M-block
       float s = -INFINITY;
       const bool ok = lane < T && lane < klen && (n != m || lane <= qr);
@@ -97,10 +101,21 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(PlanTables pt, AttnArgs a
       mrun[rr] = mnew;
 #pragma unroll
       for (int c = 0; c < C; ++c) o[rr][c] *= alpha;
-      for (int j = 0; j < T; ++j) {
-        const float pj = __shfl(p, j, 64);
+      // the weights go through LDS (one wavefront writes and reads its own
+      // row, in order) and come back four at a time to every lane
+      if (lane < T) Ps[w][lane] = p;
+#pragma unroll 4
+      for (int j = 0; j < T; j += 4) {
+        const float4 p4 = *reinterpret_cast<const float4*>(&Ps[w][j]);
 #pragma unroll
-        for (int c = 0; c < C; ++c) o[rr][c] = fmaf(pj, Vs[j * D + lane + 64 * c], o[rr][c]);
+        for (int c = 0; c < C; ++c) {
+          float acc = o[rr][c];
+          acc = fmaf(p4.x, Vs[j * D + lane + 64 * c], acc);
+          acc = fmaf(p4.y, Vs[(j + 1) * D + lane + 64 * c], acc);
+          acc = fmaf(p4.z, Vs[(j + 2) * D + lane + 64 * c], acc);
+          acc = fmaf(p4.w, Vs[(j + 3) * D + lane + 64 * c], acc);
+          o[rr][c] = acc;
+        }
       }
     }
   }
