@@ -272,38 +272,100 @@ def _weighted_rows(P: np.ndarray, allowed: np.ndarray, vv: np.ndarray) -> np.nda
     return out
 
 
-def attention(lay: Layout, q, k, v, la, ca, scale=None, heads=None, rows=None) -> np.ndarray:
+def _row_groups(lay: Layout, rows: np.ndarray):
+    """Split global token rows into groups of one prompt and one query tile
+    (M-block): yields (prompt b, positions into `rows`, prompt-relative rows)."""
+    tile_of = np.empty(len(rows), dtype=np.int64)
+    prompt_of = np.empty(len(rows), dtype=np.int64)
+    for s in lay.segs:
+        sel = (rows >= s.start) & (rows < s.start + s.length)
+        tile_of[sel] = s.tile_base + (rows[sel] - s.start) // lay.tile
+        prompt_of[sel] = s.prompt
+    order = np.argsort(tile_of, kind="stable")
+    bounds = np.nonzero(np.diff(tile_of[order]))[0] + 1
+    for grp in np.split(order, bounds):
+        if grp.size:
+            b = int(prompt_of[grp[0]])
+            yield b, grp, rows[grp] - lay.prompt_span(b)[0]
+
+
+def _attend_group(lay: Layout, q, kk, vv, la, ca, head: int, b: int, rel_rows, scale,
+                  cache: dict) -> np.ndarray:
+    """Output rows of one group (rows of one M-block of prompt b) for one query
+    head.  kk, vv: the prompt's K and V rows of the head's kv head, float64.
+    Scores are formed for the keys some row of the group may see (the union of
+    the rows' masks); every other key has probability 0 for all of them."""
+    p0, _ = lay.prompt_span(b)
+    allowed = mask_rows(lay, la, ca, head, b, rel_rows, cache)
+    keys = np.nonzero(allowed.any(axis=0))[0]
+    if keys.size and keys[-1] - keys[0] + 1 == keys.size:
+        ksel = slice(int(keys[0]), int(keys[-1]) + 1)      # a contiguous range: no copy
+    else:
+        ksel = keys
+    qr = np.asarray(q[p0 + rel_rows, head, :], dtype=np.float64)
+    s = (qr @ kk[ksel].T) * scale
+    am = allowed[:, ksel]
+    P = masked_softmax_rows(s, am)
+    vs = vv[ksel]
+    if np.isfinite(vs).all():
+        return P @ vs                      # P is 0 outside each row's mask
+    return _weighted_rows(P, am, vs)       # non-finite V: read the allowed keys only
+
+
+def attention(lay: Layout, q, k, v, la, ca, scale=None, heads=None, rows=None,
+              workers: int = 1) -> np.ndarray:
     """O[t, h, :] in float64.
 
     q: [L, Hq, D]; k, v: [L, Hkv, D]; la, ca: uint8 buffers.  With `rows`
     (global token indices) only those rows are computed and the result is
-    [len(rows), Hq, D]; with `heads` only those heads are filled."""
+    [len(rows), Hq, D]; with `heads` only those heads are filled.  Rows are
+    handled in groups that share a query tile, one (head, prompt) at a time;
+    `workers` threads take (head, prompt) pairs in parallel."""
     L, hq, D = q.shape
-    heads = range(hq) if heads is None else heads
-    if rows is None:
-        out = np.zeros((L, hq, D), dtype=np.float64)
-        for b in range(lay.num_prompts):
+    hkv = k.shape[1]
+    heads = list(range(hq)) if heads is None else list(heads)
+    sc = 1.0 / np.sqrt(D) if scale is None else float(scale)
+    want = np.arange(L, dtype=np.int64) if rows is None else np.asarray(rows, dtype=np.int64)
+    out = np.zeros((len(want), hq, D), dtype=np.float64)
+    groups: dict[int, list] = {}
+    for b, pos, rel in _row_groups(lay, want):
+        groups.setdefault(b, []).append((pos, rel))
+    kv_cache: dict = {}
+
+    def kv(b, g):
+        if (b, g) not in kv_cache:
             p0, p1 = lay.prompt_span(b)
-            vv = {}
-            for h in heads:
-                g = _kv_head(h, hq, k.shape[1])
-                if g not in vv:
-                    vv[g] = np.asarray(v[p0:p1, g, :], dtype=np.float64)
-                for c0 in range(0, p1 - p0, lay.tile):
-                    rr = np.arange(c0, min(c0 + lay.tile, p1 - p0))
-                    P, allowed = _probs_and_mask(lay, q, k, la, ca, h, b, rr, scale)
-                    out[p0 + rr, h, :] = _weighted_rows(P, allowed, vv[g])
-        return out
-    rows = np.asarray(rows, dtype=np.int64)
-    out = np.zeros((len(rows), hq, D), dtype=np.float64)
-    for n, t in enumerate(rows):
-        b = next(bb for bb in range(lay.num_prompts)
-                 if lay.prompt_span(bb)[0] <= t < lay.prompt_span(bb)[1])
-        p0, p1 = lay.prompt_span(b)
+            kv_cache[(b, g)] = (np.asarray(k[p0:p1, g, :], dtype=np.float64),
+                                np.asarray(v[p0:p1, g, :], dtype=np.float64))
+        return kv_cache[(b, g)]
+
+    # the float64 K/V copies are made up front, once per (prompt, kv head)
+    for b in groups:
         for h in heads:
-            g = _kv_head(h, hq, k.shape[1])
-            P, allowed = _probs_and_mask(lay, q, k, la, ca, h, b, [t - p0], scale)
-            out[n, h, :] = _weighted_rows(P, allowed, np.asarray(v[p0:p1, g, :], dtype=np.float64))[0]
+            kv(b, _kv_head(h, hq, hkv))
+
+    def job(h, b, part):
+        kk, vv = kv(b, _kv_head(h, hq, hkv))
+        cache: dict = {}
+        for pos, rel in part:
+            out[pos, h, :] = _attend_group(lay, q, kk, vv, la, ca, h, b, rel, sc, cache)
+
+    # jobs: (head, prompt, a run of consecutive row groups)
+    per_job = 1 if workers <= 1 else 8
+    jobs = [(h, b, grp[i:i + per_job] if workers > 1 else grp)
+            for h in heads for b, grp in groups.items()
+            for i in (range(0, len(grp), per_job) if workers > 1 else [0])]
+    if workers <= 1 or len(jobs) <= 1:
+        for h, b, part in jobs:
+            job(h, b, part)
+    else:
+        # one BLAS thread per worker: the workers are the parallelism
+        from concurrent.futures import ThreadPoolExecutor
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1, user_api="blas"):
+            with ThreadPoolExecutor(max_workers=workers) as ex:
+                for f in [ex.submit(job, *jb) for jb in jobs]:
+                    f.result()
     return out
 
 
