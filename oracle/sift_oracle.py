@@ -95,6 +95,13 @@ def read_bit(buf, byte_offset: int, b: int) -> int:
     return (byte >> (7 - (b & 7))) & 1
 
 
+def read_bits(buf, byte_offset: int, positions) -> np.ndarray:
+    """read_bit at every position of an integer array (same rule, vectorised)."""
+    b = np.asarray(positions, dtype=np.int64)
+    byte = np.asarray(buf, dtype=np.uint8)[byte_offset + (b >> 3)].astype(np.int64)
+    return ((byte >> (7 - (b & 7))) & 1).astype(bool)
+
+
 # ----------------------------------------------------------------------------
 # Prompt layout
 # ----------------------------------------------------------------------------
@@ -165,7 +172,7 @@ class Layout:
 
 
 def _page_bits(buf, off: int, n: int) -> np.ndarray:
-    return np.array([read_bit(buf, off, b) for b in range(n)], dtype=bool)
+    return read_bits(buf, off, np.arange(n))
 
 
 def _tile_row(lay: Layout, la, ca, head: int, b: int, seg_index: int, i: int,
@@ -200,10 +207,10 @@ def _tile_row(lay: Layout, la, ca, head: int, b: int, seg_index: int, i: int,
     else:
         # local attention: tiles j <= i of the same document (Section 4.1)
         off = me.la_offset + head * la_num_bytes(me.pages)
-        for j in range(i + 1):
-            bit = 1 if j == i else read_bit(la, off, la_bit_position(i, j))
-            lo, hi = j * lay.tile, min((j + 1) * lay.tile, me.length)
-            row[a + lo:a + hi] = bool(bit)
+        bits = read_bits(la, off, la_bit_position(i, 0) + np.arange(i + 1))
+        bits[i] = True                      # the diagonal tile, whatever its bit
+        lo, hi = a, a + min((i + 1) * lay.tile, me.length)
+        row[lo:hi] = np.repeat(bits, lay.tile)[:hi - lo]
     return row
 
 
@@ -374,18 +381,25 @@ def attention(lay: Layout, q, k, v, la, ca, scale=None, heads=None, rows=None,
 # ----------------------------------------------------------------------------
 
 
-def _key_tile_any(lay: Layout, b: int, keyrow: np.ndarray) -> list[int]:
-    """Global tile numbers of the prompt's key tiles that hold a True."""
+def _prompt_key_tiles(lay: Layout, b: int) -> tuple[np.ndarray, np.ndarray]:
+    """(prompt-relative first token, global tile number) of the prompt's tiles."""
     p0, _ = lay.prompt_span(b)
     starts, ids = [], []
     for s in lay.prompt_segs(b):
         for i in range(s.pages):
             starts.append(s.start - p0 + i * lay.tile)
             ids.append(s.tile_base + i)
-    if not starts:
+    return np.asarray(starts, dtype=np.int64), np.asarray(ids, dtype=np.int64)
+
+
+def _key_tile_any(lay: Layout, b: int, keyrow: np.ndarray, tiles=None) -> list[int]:
+    """Global tile numbers of the prompt's key tiles that hold a True.
+    `tiles` may pass _prompt_key_tiles(lay, b) computed once."""
+    starts, ids = _prompt_key_tiles(lay, b) if tiles is None else tiles
+    if starts.size == 0:
         return []
-    hit = np.logical_or.reduceat(keyrow, np.asarray(starts))
-    return [n for n, x in zip(ids, hit) if x]
+    hit = np.logical_or.reduceat(keyrow, starts)
+    return ids[hit].tolist()
 
 
 def tile_lists(lay: Layout, la, ca, heads=None, mblocks=None, exhaustive: bool = False):
@@ -401,14 +415,17 @@ def tile_lists(lay: Layout, la, ca, heads=None, mblocks=None, exhaustive: bool =
     mblocks = range(lay.num_tiles) if mblocks is None else mblocks
     res = {}
     cache: dict = {}
+    tiles: dict = {}
     for m in mblocks:
         seg, i, a, n = lay.tile_span(m)
         b = seg.prompt
+        if b not in tiles:
+            tiles[b] = _prompt_key_tiles(lay, b)
         p0, _ = lay.prompt_span(b)
         rows = np.arange(a - p0, a - p0 + n) if exhaustive else np.array([a - p0 + n - 1])
         for h in heads:
             msk = mask_rows(lay, la, ca, h, b, rows, cache).any(axis=0)
-            res[(h, m)] = _key_tile_any(lay, b, msk)
+            res[(h, m)] = _key_tile_any(lay, b, msk, tiles[b])
     return res
 
 

@@ -441,3 +441,14 @@ def test_useful_flops_dense_closed_form():
     lists = O.tile_lists(lay, la, ca)
     # dense causal cells: L(L+1)/2 with L = 14
     assert O.useful_flops(lay, lists, 8) == 4 * 8 * 14 * 15 // 2
+
+
+def test_vectorised_bit_reader_equals_scalar_reader():
+    """read_bits (used to build masks) gives read_bit's answer at every
+    position, offsets included."""
+    rng = np.random.default_rng(12)
+    buf = rng.integers(0, 256, size=40, dtype=np.uint8)
+    for off in (0, 3, 17):
+        pos = np.arange((40 - off) * 8)
+        want = [O.read_bit(buf, off, int(b)) for b in pos]
+        assert O.read_bits(buf, off, pos).astype(int).tolist() == want
