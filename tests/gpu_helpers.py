@@ -98,3 +98,9 @@ def sample_rows(wl: W.Workload, n: int, seed: int = 0) -> np.ndarray:
 
 def max_abs(a, b) -> float:
     return float(np.max(np.abs(np.asarray(a, np.float64) - np.asarray(b, np.float64)))) if np.size(a) else 0.0
+
+
+def workers() -> int:
+    """Threads for the oracle: the host cores this process may use, at most 16."""
+    import os
+    return max(1, min(16, len(os.sched_getaffinity(0))))

@@ -70,3 +70,25 @@ def test_slice_reduces_to_textbook_attention():
           "w_post": np.ones(hidden), "Wg": np.zeros((5, hidden)), "Wu": np.zeros((5, hidden)),
           "Wd": np.zeros((hidden, 5))}
     assert np.abs(LO.layer_slice(lay, x, w0, la, ca, pos, f, 1, 1, d) - x).max() == 0.0
+
+
+def test_mlp_composition_hand_worked():
+    """The MLP branch against a case worked by hand (golden
+    layer_mlp_example.json): silu on the gate, the up projection as the
+    other factor, w_post applied after the second norm, and the norm taken
+    of x1 (after the attention residual).  Each wrong reading listed in the
+    fixture lands far outside the tolerance."""
+    import json
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "layer_mlp_example.json")
+    g = json.load(open(path))
+    lay = O.Layout([0, 1], [0, 1], 16, 1)          # one prompt: a 1-token query
+    w = {k: np.asarray(g[k], dtype=np.float64)
+         for k in ("w_in", "Wqkv", "Wo", "w_post", "Wg", "Wu", "Wd")}
+    x = np.asarray(g["x"], dtype=np.float64)
+    out = LO.layer_slice(lay, x, w, np.zeros(0, np.uint8), np.zeros(0, np.uint8), np.array([0]),
+                         np.array([1.0], dtype=np.float32), 1, 1, 2)
+    want = np.asarray(g["expected"], dtype=np.float64)
+    assert np.abs(out - want).max() < 1e-12
+    for wrong in g["wrong_readings"].values():
+        assert abs(wrong - want[0, 0]) > 1e-2

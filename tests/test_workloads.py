@@ -102,3 +102,37 @@ def test_ragged_layout():
             assert s.length % 64 == 0 and 256 <= s.length <= 2048
         else:
             assert 64 <= s.length <= 512
+
+
+@pytest.mark.parametrize("tile", [16, 32, 64, 128])
+def test_scramble_changes_only_ignored_bits(tile):
+    """The scrambler clears stored diagonal bits of every other vector and
+    sets every padding bit; the oracle, which ignores both (Sections 4.1,
+    4.3), gives the same lists and outputs on the scrambled bits."""
+    wl = W.custom([[300, 64, 129, 75], [5], [1, 64, 0], [200, 131, 70]], tile=tile, hq=4, hkv=2,
+                  d=16, dtype="f32", seed=tile, p_la=0.4, p_ca=0.3)
+    ws = W.scramble_ignored_bits(wl, seed=1)
+    assert ws.la.shape == wl.la.shape and ws.ca.shape == wl.ca.shape
+    lay = O.Layout(wl.seg_offsets, wl.prompt_seg_ptr, wl.tile, wl.hq)
+    # walk the vectors: count cleared diagonals and set padding bits
+    cleared = padded = 0
+    for s in lay.segs:
+        if s.is_query:
+            continue
+        P = s.pages
+        for h in range(wl.hq):
+            off = s.la_offset + h * O.la_num_bytes(P)
+            bits = np.unpackbits(ws.la[off:off + O.la_num_bytes(P)], bitorder="big")
+            diag = [O.la_bit_position(i, i) for i in range(P)]
+            cleared += int((bits[diag] == 0).all())
+            assert (bits[P * (P + 1) // 2:] == 1).all()
+            padded += bits.size - P * (P + 1) // 2
+            coff = s.ca_offset + h * O.ca_num_bytes(P)
+            cb = np.unpackbits(ws.ca[coff:coff + O.ca_num_bytes(P)], bitorder="big")
+            assert (cb[P:] == 1).all()
+            padded += cb.size - P
+    assert cleared > 0 and padded > 0
+    assert O.tile_lists(lay, ws.la, ws.ca) == O.tile_lists(lay, wl.la, wl.ca)
+    a = O.attention(lay, wl.q, wl.k, wl.v, wl.la, wl.ca)
+    b = O.attention(lay, ws.q, ws.k, ws.v, ws.la, ws.ca)
+    np.testing.assert_array_equal(a, b)

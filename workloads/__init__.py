@@ -26,7 +26,7 @@ from dataclasses import dataclass, field, replace
 
 import numpy as np
 
-__all__ = ["Workload", "make", "CONFIGS", "all_ones", "bf16_round", "pack_msb", "layer_weights",
+__all__ = ["Workload", "make", "CONFIGS", "all_ones", "scramble_ignored_bits", "custom", "bf16_round", "pack_msb", "layer_weights",
            "layer_input", "rope_inv_freq", "prompt_positions"]
 
 
@@ -312,6 +312,42 @@ def all_ones(wl: Workload) -> Workload:
     la = np.concatenate(la_parts) if la_parts else np.zeros(0, np.uint8)
     ca = np.concatenate(ca_parts) if ca_parts else np.zeros(0, np.uint8)
     return replace(wl, name=wl.name + "_dense", la=la, ca=ca, meta={**wl.meta, "all_ones": True})
+
+
+def scramble_ignored_bits(wl: Workload, seed: int = 0) -> Workload:
+    """The same input with every bit the format says to ignore changed.
+
+    Diagonal tiles are always computed, whatever their stored bit says, and
+    the bits after the last tile of a vector (padding to a whole byte) carry
+    nothing (Sections 4.1, 4.3).  Here the stored diagonal bits of every
+    other vector (in buffer order) are cleared and those of the rest drawn
+    at random, and every padding bit of every LA and CA vector is set."""
+    rng = np.random.default_rng(seed)
+    la = wl.la.copy()
+    ca = wl.ca.copy()
+    la_off = ca_off = 0
+    ordinal = 0
+    for b in range(len(wl.prompt_seg_ptr) - 1):
+        s0, s1 = int(wl.prompt_seg_ptr[b]), int(wl.prompt_seg_ptr[b + 1]) - 1
+        for s in range(s0, s1):               # documents; the last segment is the query
+            P = _pages(int(wl.seg_offsets[s + 1] - wl.seg_offsets[s]), wl.tile)
+            n_la, n_ca = P * (P + 1) // 2, P
+            b_la, b_ca = -(-n_la // 8), -(-n_ca // 8)
+            diag = np.array([i * (i + 1) // 2 + i for i in range(P)], dtype=np.int64)
+            for _ in range(wl.hq):
+                bits = np.unpackbits(la[la_off:la_off + b_la], bitorder="big")
+                bits[diag] = 0 if ordinal % 2 == 0 else rng.integers(0, 2, size=P)
+                bits[n_la:] = 1
+                la[la_off:la_off + b_la] = np.packbits(bits, bitorder="big")
+                cb = np.unpackbits(ca[ca_off:ca_off + b_ca], bitorder="big")
+                cb[n_ca:] = 1
+                ca[ca_off:ca_off + b_ca] = np.packbits(cb, bitorder="big")
+                la_off += b_la
+                ca_off += b_ca
+                ordinal += 1
+    assert la_off == la.size and ca_off == ca.size
+    return replace(wl, name=wl.name + "_scrambled", la=la, ca=ca,
+                   meta={**wl.meta, "ignored_bits_scrambled": seed})
 
 
 def custom(seg_lens_per_prompt, tile, hq, hkv, d, dtype, seed=0, p_la=0.3, p_ca=0.3) -> Workload:
