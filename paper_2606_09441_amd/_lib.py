@@ -138,6 +138,8 @@ def _torch():
 
 def tensor_desc(t) -> SiftTensor:
     torch = _torch()
+    if not getattr(t, "is_cuda", False):
+        raise SiftError("tensor_desc", 4, "tensors must be in GPU memory")
     if t.dim() != 3:
         raise ValueError("expected a [tokens, heads, head_dim] tensor")
     if not t.is_contiguous():
@@ -149,6 +151,50 @@ def tensor_desc(t) -> SiftTensor:
     else:
         raise ValueError(f"unsupported dtype {t.dtype}")
     return SiftTensor(t.data_ptr(), dt, t.shape[0], t.shape[1], t.shape[2])
+
+
+def require(fn: str, t, name: str, dtype: str, min_numel: int, device=None) -> None:
+    """Check a device buffer before its pointer goes to the library, which
+    cannot see buffer sizes: a GPU tensor (on `device` when given), of
+    `dtype` ("uint8", "int32", "float32"), contiguous, with at least
+    min_numel elements.  Raises SiftError otherwise."""
+    torch = _torch()
+    want = {"uint8": torch.uint8, "int32": torch.int32, "float32": torch.float32}[dtype]
+    if t is None:
+        if min_numel > 0:
+            raise SiftError(fn, 1, f"{name} is required")
+        return
+    if not isinstance(t, torch.Tensor):
+        raise SiftError(fn, 4, f"{name} must be a torch tensor")
+    if t.dtype != want:
+        raise SiftError(fn, 4, f"{name} must be {dtype}, not {t.dtype}")
+    if not t.is_contiguous():
+        raise SiftError(fn, 2, f"{name} must be contiguous")
+    if t.numel() < min_numel:
+        raise SiftError(fn, 5, f"{name} holds {t.numel()} elements, needs {min_numel}")
+    if not t.is_cuda:
+        raise SiftError(fn, 4, f"{name} must be a GPU tensor")
+    if device is not None and t.device != device:
+        raise SiftError(fn, 7, f"{name} is on {t.device}, the plan on {device}")
+
+
+def bitmap_bytes(seg_offsets, prompt_seg_ptr, num_q_heads: int, tile: int) -> tuple[int, int]:
+    """(LA bytes, CA bytes) the bit-vector buffers of a layout hold, from the
+    library (sift_extract_sizes over the layout's documents in order)."""
+    so = np.asarray(seg_offsets, dtype=np.int64)
+    ps = np.asarray(prompt_seg_ptr, dtype=np.int64)
+    lens = [int(so[s + 1] - so[s]) for b in range(len(ps) - 1)
+            for s in range(int(ps[b]), int(ps[b + 1]) - 1)]
+    if not lens:
+        return 0, 0
+    if min(lens) < 1:
+        raise SiftError("bitmap_bytes", 3, "documents must hold at least one token")
+    offs = np.ascontiguousarray(np.concatenate([[0], np.cumsum(lens)]).astype(np.int32))
+    la, ca = ctypes.c_size_t(), ctypes.c_size_t()
+    check("sift_extract_sizes", lib().sift_extract_sizes(len(lens), offs.ctypes.data_as(_P),
+                                                         num_q_heads, tile, ctypes.byref(la),
+                                                         ctypes.byref(ca), None))
+    return la.value, ca.value
 
 
 def layout_struct(seg_offsets, prompt_seg_ptr):
@@ -179,6 +225,8 @@ class Plan:
         check("sift_plan_create", lib().sift_plan_create(ctypes.byref(lay), num_q_heads, num_kv_heads,
                                                          head_dim, tile, ctypes.byref(h)))
         self._h = h
+        torch = _torch()
+        self.device = torch.device("cuda", torch.cuda.current_device())
         inf = SiftPlanInfo()
         check("sift_plan_get_info", lib().sift_plan_get_info(self._h, ctypes.byref(inf)))
         self.info = {name: getattr(inf, name) for name, _ in SiftPlanInfo._fields_}
@@ -200,14 +248,23 @@ class Plan:
     def __exit__(self, *exc):
         self.close()
 
+    def _bits(self, fn, la, ca):
+        require(fn, la, "local_bitmap", "uint8", self.info["la_bytes"], self.device)
+        require(fn, ca, "cross_bitmap", "uint8", self.info["ca_bytes"], self.device)
+
     def decode(self, la, ca, row_ptr=None, col_idx=None, stream=None):
         """Decoded lists (Section 5.1) as device int32 tensors (row_ptr, col_idx)."""
         torch = _torch()
+        self._bits("sift_decode_tiles", la, ca)
         dev = la.device
         if row_ptr is None:
             row_ptr = torch.empty(self.info["num_rows"] + 1, dtype=torch.int32, device=dev)
         if col_idx is None:
             col_idx = torch.empty(max(1, self.info["list_capacity"]), dtype=torch.int32, device=dev)
+        require("sift_decode_tiles", row_ptr, "row_ptr", "int32", self.info["num_rows"] + 1,
+                self.device)
+        require("sift_decode_tiles", col_idx, "col_idx", "int32", self.info["list_capacity"],
+                self.device)
         check("sift_decode_tiles", lib().sift_decode_tiles(
             self._h, _ptr(la), _ptr(ca), _ptr(row_ptr), _ptr(col_idx), col_idx.numel(),
             _stream_ptr(stream)))
@@ -216,6 +273,9 @@ class Plan:
     def attention(self, q, k, v, row_ptr, col_idx, scale=None, out=None, out_dtype=None, stream=None):
         """Sparse attention over given lists (Section 5.2)."""
         torch = _torch()
+        require("sift_sparse_attention", row_ptr, "row_ptr", "int32", self.info["num_rows"] + 1,
+                self.device)
+        require("sift_sparse_attention", col_idx, "col_idx", "int32", 0, self.device)
         if out is None:
             out = torch.empty(q.shape, dtype=out_dtype or q.dtype, device=q.device)
         qd, kd, vd, od = tensor_desc(q), tensor_desc(k), tensor_desc(v), tensor_desc(out)
@@ -227,6 +287,7 @@ class Plan:
 
     def decode_internal(self, la, ca, stream=None):
         """Decode into the plan's own scratch (sift_plan_decode)."""
+        self._bits("sift_plan_decode", la, ca)
         check("sift_plan_decode", lib().sift_plan_decode(self._h, _ptr(la), _ptr(ca),
                                                          _stream_ptr(stream)))
 
@@ -244,6 +305,7 @@ class Plan:
     def run(self, q, k, v, la, ca, scale=None, out=None, out_dtype=None, stream=None):
         """Decode + attention for one layer (sift_plan_run)."""
         torch = _torch()
+        self._bits("sift_plan_run", la, ca)
         if out is None:
             out = torch.empty(q.shape, dtype=out_dtype or q.dtype, device=q.device)
         qd, kd, vd, od = tensor_desc(q), tensor_desc(k), tensor_desc(v), tensor_desc(out)
@@ -257,6 +319,9 @@ class Plan:
         """Decode + attention with K/V in a page pool (sift_plan_run_paged):
         k_pages/v_pages [num_pages * T, Hkv, D], page_table int32 [num_tiles]."""
         torch = _torch()
+        self._bits("sift_plan_run_paged", la, ca)
+        require("sift_plan_run_paged", page_table, "page_table", "int32", self.info["num_tiles"],
+                self.device)
         if out is None:
             out = torch.empty(q.shape, dtype=out_dtype or q.dtype, device=q.device)
         qd, kd, vd, od = tensor_desc(q), tensor_desc(k_pages), tensor_desc(v_pages), tensor_desc(out)
@@ -270,6 +335,7 @@ class Plan:
 def sparse_prefill(q, k, v, seg_offsets, prompt_seg_ptr, la, ca, tile=64, out=None, stream=None):
     """One-shot sift_sparse_prefill: plan, decode, attention, wait, free."""
     torch = _torch()
+    _check_bits("sift_sparse_prefill", q, la, ca, seg_offsets, prompt_seg_ptr, tile)
     if out is None:
         out = torch.empty_like(q)
     lay, keep = layout_struct(seg_offsets, prompt_seg_ptr)
@@ -278,6 +344,15 @@ def sparse_prefill(q, k, v, seg_offsets, prompt_seg_ptr, la, ca, tile=64, out=No
         ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), ctypes.byref(lay), _ptr(la), _ptr(ca),
         tile, ctypes.byref(od), _stream_ptr(stream)))
     return out
+
+
+def _check_bits(fn, q, la, ca, seg_offsets, prompt_seg_ptr, tile):
+    """The bit-vector buffers of a one-shot call, against the layout's sizes."""
+    if not getattr(q, "is_cuda", False):
+        raise SiftError(fn, 4, "q must be a GPU tensor")
+    la_n, ca_n = bitmap_bytes(seg_offsets, prompt_seg_ptr, q.shape[1], tile)
+    require(fn, la, "local_bitmap", "uint8", la_n, q.device)
+    require(fn, ca, "cross_bitmap", "uint8", ca_n, q.device)
 
 
 def workspace_bytes(seg_offsets, prompt_seg_ptr, num_q_heads, num_kv_heads, head_dim, tile=64):
@@ -296,11 +371,13 @@ def sparse_prefill_ex(q, k, v, seg_offsets, prompt_seg_ptr, la, ca, tile=64, sca
     workspace: a uint8 device tensor of at least workspace_bytes(...) bytes
     (allocated here when None)."""
     torch = _torch()
+    _check_bits("sift_sparse_prefill_ex", q, la, ca, seg_offsets, prompt_seg_ptr, tile)
     if out is None:
         out = torch.empty_like(q)
+    n = workspace_bytes(seg_offsets, prompt_seg_ptr, q.shape[1], k.shape[1], q.shape[2], tile)
     if workspace is None:
-        n = workspace_bytes(seg_offsets, prompt_seg_ptr, q.shape[1], k.shape[1], q.shape[2], tile)
         workspace = torch.empty(max(n, 1), dtype=torch.uint8, device=q.device)
+    require("sift_sparse_prefill_ex", workspace, "workspace", "uint8", n, q.device)
     lay, keep = layout_struct(seg_offsets, prompt_seg_ptr)
     qd, kd, vd, od = tensor_desc(q), tensor_desc(k), tensor_desc(v), tensor_desc(out)
     check("sift_sparse_prefill_ex", lib().sift_sparse_prefill_ex(
@@ -337,6 +414,7 @@ def extract_bits(q, k, doc_offsets, tile=64, alpha=0.001, beta=0.01, gamma=0.1, 
     if workspace is None or workspace.numel() < ws_n:
         workspace = torch.empty(max(ws_n, 1), dtype=torch.uint8, device=q.device)
     qd, kd = tensor_desc(q), tensor_desc(k)
+    require("sift_extract_bits", workspace, "workspace", "uint8", ws_n, q.device)
     check("sift_extract_bits", lib().sift_extract_bits(
         ctypes.byref(qd), ctypes.byref(kd), len(offs) - 1, offs.ctypes.data_as(_P), tile,
         float(alpha), float(beta), float(gamma), ctypes.c_float(0.0 if scale is None else scale),
@@ -347,6 +425,8 @@ def extract_bits(q, k, doc_offsets, tile=64, alpha=0.001, beta=0.01, gamma=0.1, 
 def rope_(q, k, positions, inv_freq, stream=None):
     """In-place rotary embedding of bf16 q and k (sift_rope)."""
     qd, kd = tensor_desc(q), tensor_desc(k)
+    require("sift_rope", positions, "positions", "int32", q.shape[0], q.device)
+    require("sift_rope", inv_freq, "inv_freq", "float32", q.shape[2] // 2, q.device)
     check("sift_rope", lib().sift_rope(ctypes.byref(qd), ctypes.byref(kd), _ptr(positions),
                                        _ptr(inv_freq), _stream_ptr(stream)))
     return q, k
