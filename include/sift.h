@@ -123,7 +123,7 @@ const char* sift_status_string(int32_t status);
  *   layout           host layout, read only during the call
  *   num_q_heads      Hq >= 1;  num_kv_heads: Hkv >= 1, Hq % Hkv == 0
  *   head_dim         D: 64 or 128
- *   tile             T: 16, 32, 64 or 128 (bf16 attention: 64 or 128;
+ *   tile             T: 16, 32, 64 or 128 (bf16 attention: any of them;
  *                    fp32 attention: 16, 32 or 64)
  *   plan_out         receives the plan; the caller frees it with
  *                    sift_plan_destroy.
@@ -134,15 +134,16 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
                              int32_t num_kv_heads, int32_t head_dim,
                              int32_t tile, sift_plan** plan_out);
 
-/* Free a plan and its device memory (synchronises the device first).
- * NULL is accepted. */
+/* Free a plan and its device memory (waits first for the stream of the
+ * plan's last enqueued work).  NULL is accepted. */
 sift_status sift_plan_destroy(sift_plan* plan);
 
 /* Copy the plan's sizes into *info. */
 sift_status sift_plan_get_info(const sift_plan* plan, sift_plan_info* info);
 
 /*
- * Decoding (Section 5.1): expand the bit vectors into the packed lists.
+ * Decoding (Section 5.1) with a plan: expand the bit vectors into the packed
+ * lists.
  *   local_bitmap, cross_bitmap   device, la_bytes / ca_bytes of the plan
  *   row_ptr      device int32 [num_rows + 1], written: exclusive prefix sum
  *                of the per-row counts; row_ptr[num_rows] = nnz
@@ -152,22 +153,49 @@ sift_status sift_plan_get_info(const sift_plan* plan, sift_plan_info* info);
  * Uses the plan's scratch for the counts, and also leaves there the per-unit
  * merged step lists (see sift_plan_attention).
  */
-sift_status sift_decode_tiles(sift_plan* plan, const uint8_t* local_bitmap,
-                              const uint8_t* cross_bitmap, int32_t* row_ptr,
-                              int32_t* col_idx, int64_t col_capacity,
-                              void* stream);
+sift_status sift_plan_decode_tiles(sift_plan* plan, const uint8_t* local_bitmap,
+                                   const uint8_t* cross_bitmap, int32_t* row_ptr,
+                                   int32_t* col_idx, int64_t col_capacity, void* stream);
+
+/*
+ * Decoding (Section 5.1) without a plan: the layout, the two bit vectors
+ * and the tile size in, the packed lists out, with caller-owned scratch.
+ *   layout       host layout, read only during the call
+ *   local_bitmap, cross_bitmap   device, in the layout above (their sizes
+ *                follow from the layout, T and num_q_heads: Section 4.3)
+ *   tile         T: 16, 32, 64 or 128;  num_q_heads: Hq >= 1
+ *   row_ptr, col_idx, col_capacity   as in sift_plan_decode_tiles; the
+ *                capacity must be >= Hq * (causal tiles of all prompts),
+ *                the list_capacity of a plan of this layout
+ *   workspace    device, 256-byte aligned, at least
+ *                sift_decode_workspace_bytes(layout, num_q_heads, tile)
+ *                bytes, owned by the caller: the decode's tables and scratch
+ * The tables are copied into the workspace on `stream` from pinned host
+ * memory the library keeps; the call returns once the work is enqueued,
+ * without waiting for the stream.  The workspace must stay allocated until
+ * that work is done; calls sharing a workspace must be ordered.
+ * Errors: SIFT_E_NULL, SIFT_E_LAYOUT, SIFT_E_SHAPE, SIFT_E_UNSUPPORTED,
+ *   SIFT_E_CAPACITY (col_capacity or workspace too small), SIFT_E_HIP; all
+ *   but SIFT_E_HIP before anything is enqueued.
+ */
+sift_status sift_decode_workspace_bytes(const sift_layout* layout, int32_t num_q_heads,
+                                        int32_t tile, size_t* bytes);
+sift_status sift_decode_tiles(const sift_layout* layout, const uint8_t* local_bitmap,
+                              const uint8_t* cross_bitmap, int32_t tile, int32_t num_q_heads,
+                              int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
+                              void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * Decoding into the plan's own scratch (the lists and the per-unit merged
  * step lists the bf16 attention kernel walks), as the first step of
- * sift_plan_run.  Same bitmaps and errors as sift_decode_tiles.
+ * sift_plan_run.  Same bitmaps and errors as sift_plan_decode_tiles.
  */
 sift_status sift_plan_decode(sift_plan* plan, const uint8_t* local_bitmap,
                              const uint8_t* cross_bitmap, void* stream);
 
 /*
  * Sparse attention (Section 5.2) over the lists the last sift_plan_decode
- * (or sift_plan_run, or sift_decode_tiles) on this plan produced: the
+ * (or sift_plan_run, or sift_plan_decode_tiles) on this plan produced: the
  * second step of sift_plan_run.  Tensors, scale and output as in
  * sift_sparse_attention.  SIFT_E_PLAN (bf16 inputs) when the last decode on
  * the plan was the one of sift_plan_run_paged: its step lists index a page
@@ -181,8 +209,9 @@ sift_status sift_plan_attention(sift_plan* plan, const sift_tensor* q, const sif
  * Sparse attention (Section 5.2) over given lists: for every (h, M-block m),
  * out rows of m = softmax over the keys of the listed tiles (causal inside
  * the diagonal tile, length-masked in partial tiles) times V.
- *   q, k, v      device tensors; dtype both SIFT_BF16 (needs T = 64 and
- *                D = 128: MFMA kernel) or both SIFT_F32 (any supported T, D)
+ *   q, k, v      device tensors; dtype both SIFT_BF16 (MFMA kernel: D =
+ *                128, T = 16, 32, 64 or 128) or both SIFT_F32 (VALU kernel:
+ *                D = 64 or 128, T = 16, 32 or 64)
  *   row_ptr, col_idx   device lists in the format sift_decode_tiles writes,
  *                col_capacity entries of col_idx readable.  Entries outside
  *                the M-block's prompt or after the M-block are skipped;
@@ -238,8 +267,14 @@ sift_status sift_plan_run_paged(sift_plan* plan, const sift_tensor* q,
 /*
  * One-shot form with the arguments of the paper's problem statement: Q, K,
  * V of one layer, the document layout, the two bit vectors and the tile
- * size (Sections 4 and 5).  Builds a plan, runs it on `stream` with scale
- * 1/sqrt(D), waits for the stream, and frees the plan.
+ * size (Sections 4 and 5), softmax scale 1/sqrt(D).  Stream-ordered: the
+ * scratch is taken with hipMallocAsync on `stream`, the plan's tables are
+ * copied into it on `stream` from pinned host memory the library keeps,
+ * decode and attention are enqueued, and the scratch is released with
+ * hipFreeAsync on `stream`.  The call returns once all of it is enqueued,
+ * without waiting for the stream or the device.
+ * Errors: SIFT_E_NULL, SIFT_E_SHAPE, SIFT_E_LAYOUT, SIFT_E_UNSUPPORTED,
+ *   SIFT_E_CAPACITY, all before anything is enqueued; SIFT_E_HIP.
  */
 sift_status sift_sparse_prefill(const sift_tensor* q, const sift_tensor* k,
                                 const sift_tensor* v,
@@ -257,10 +292,10 @@ sift_status sift_sparse_prefill(const sift_tensor* q, const sift_tensor* k,
  *   plan's tables and the decode and merge scratch).  Host only.
  * sift_sparse_prefill_ex: softmax_scale <= 0 means 1/sqrt(D).  workspace
  *   (device, 256-byte aligned, at least sift_workspace_bytes) is owned by
- *   the caller; the library allocates no device memory.  The call waits for
- *   `stream` (earlier work on it may still read the workspace), uploads the
- *   plan's tables into the workspace, enqueues decode and attention on
- *   `stream` and returns without waiting for them.  The workspace must stay
+ *   the caller; the library allocates no device memory.  The plan's tables
+ *   are copied into the workspace on `stream` from pinned host memory the
+ *   library keeps, decode and attention are enqueued on `stream`, and the
+ *   call returns without waiting for any of it.  The workspace must stay
  *   allocated until that work is done; calls sharing a workspace must be on
  *   one stream or otherwise ordered.
  * Errors: as sift_sparse_prefill, plus SIFT_E_NULL (no workspace),

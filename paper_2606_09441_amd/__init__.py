@@ -8,6 +8,8 @@ load the library; the first call does, and fails loudly if it is not built.
 from ._lib import (  # noqa: F401
     Plan,
     SiftError,
+    decode_tiles,
+    decode_workspace_bytes,
     default_scale,
     extract_bits,
     extract_sizes,
@@ -19,5 +21,5 @@ from ._lib import (  # noqa: F401
     workspace_bytes,
 )
 
-__all__ = ["Plan", "SiftError", "sparse_prefill", "sparse_prefill_ex", "workspace_bytes", "extract_bits", "extract_sizes", "rope_", "lib",
+__all__ = ["Plan", "SiftError", "decode_tiles", "decode_workspace_bytes", "sparse_prefill", "sparse_prefill_ex", "workspace_bytes", "extract_bits", "extract_sizes", "rope_", "lib",
            "header_functions", "default_scale"]

@@ -58,7 +58,12 @@ _SIGS = {
                                         ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(_P)]),
     "sift_plan_destroy": (ctypes.c_int, [_P]),
     "sift_plan_get_info": (ctypes.c_int, [_P, ctypes.POINTER(SiftPlanInfo)]),
-    "sift_decode_tiles": (ctypes.c_int, [_P, _P, _P, _P, _P, ctypes.c_int64, _P]),
+    "sift_plan_decode_tiles": (ctypes.c_int, [_P, _P, _P, _P, _P, ctypes.c_int64, _P]),
+    "sift_decode_workspace_bytes": (ctypes.c_int, [ctypes.POINTER(SiftLayout), ctypes.c_int32,
+                                                   ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]),
+    "sift_decode_tiles": (ctypes.c_int, [ctypes.POINTER(SiftLayout), _P, _P, ctypes.c_int32,
+                                         ctypes.c_int32, _P, _P, ctypes.c_int64, _P,
+                                         ctypes.c_size_t, _P]),
     "sift_sparse_attention": (ctypes.c_int, [_P, ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftTensor),
                                              ctypes.POINTER(SiftTensor), _P, _P, ctypes.c_int64,
                                              ctypes.c_float, ctypes.POINTER(SiftTensor), _P]),
@@ -255,17 +260,17 @@ class Plan:
     def decode(self, la, ca, row_ptr=None, col_idx=None, stream=None):
         """Decoded lists (Section 5.1) as device int32 tensors (row_ptr, col_idx)."""
         torch = _torch()
-        self._bits("sift_decode_tiles", la, ca)
+        self._bits("sift_plan_decode_tiles", la, ca)
         dev = la.device
         if row_ptr is None:
             row_ptr = torch.empty(self.info["num_rows"] + 1, dtype=torch.int32, device=dev)
         if col_idx is None:
             col_idx = torch.empty(max(1, self.info["list_capacity"]), dtype=torch.int32, device=dev)
-        require("sift_decode_tiles", row_ptr, "row_ptr", "int32", self.info["num_rows"] + 1,
+        require("sift_plan_decode_tiles", row_ptr, "row_ptr", "int32", self.info["num_rows"] + 1,
                 self.device)
-        require("sift_decode_tiles", col_idx, "col_idx", "int32", self.info["list_capacity"],
+        require("sift_plan_decode_tiles", col_idx, "col_idx", "int32", self.info["list_capacity"],
                 self.device)
-        check("sift_decode_tiles", lib().sift_decode_tiles(
+        check("sift_plan_decode_tiles", lib().sift_plan_decode_tiles(
             self._h, _ptr(la), _ptr(ca), _ptr(row_ptr), _ptr(col_idx), col_idx.numel(),
             _stream_ptr(stream)))
         return row_ptr, col_idx
@@ -333,7 +338,8 @@ class Plan:
 
 
 def sparse_prefill(q, k, v, seg_offsets, prompt_seg_ptr, la, ca, tile=64, out=None, stream=None):
-    """One-shot sift_sparse_prefill: plan, decode, attention, wait, free."""
+    """One-shot sift_sparse_prefill: stream-ordered scratch, decode and attention
+    enqueued on the stream; returns without waiting."""
     torch = _torch()
     _check_bits("sift_sparse_prefill", q, la, ca, seg_offsets, prompt_seg_ptr, tile)
     if out is None:
@@ -385,6 +391,60 @@ def sparse_prefill_ex(q, k, v, seg_offsets, prompt_seg_ptr, la, ca, tile=64, sca
         tile, ctypes.c_float(0.0 if scale is None else scale), _ptr(workspace),
         workspace.numel() * workspace.element_size(), ctypes.byref(od), _stream_ptr(stream)))
     return out
+
+
+def decode_workspace_bytes(seg_offsets, prompt_seg_ptr, num_q_heads, tile=64):
+    """Device workspace bytes of decode_tiles (sift_decode_workspace_bytes)."""
+    lay, keep = layout_struct(seg_offsets, prompt_seg_ptr)
+    n = ctypes.c_size_t()
+    check("sift_decode_workspace_bytes", lib().sift_decode_workspace_bytes(
+        ctypes.byref(lay), num_q_heads, tile, ctypes.byref(n)))
+    return n.value
+
+
+def list_capacity(seg_offsets, prompt_seg_ptr, num_q_heads, tile=64):
+    """Hq x (causal tiles of all prompts): the col_idx size that bounds any
+    decode of this layout."""
+    so = np.asarray(seg_offsets, dtype=np.int64)
+    ps = np.asarray(prompt_seg_ptr, dtype=np.int64)
+    total = 0
+    for b in range(len(ps) - 1):
+        before = 0
+        for s in range(int(ps[b]), int(ps[b + 1])):
+            P = -(-int(so[s + 1] - so[s]) // tile)
+            total += P * before + P * (P + 1) // 2
+            before += P
+    return num_q_heads * total
+
+
+def decode_tiles(seg_offsets, prompt_seg_ptr, la, ca, num_q_heads, tile=64, row_ptr=None,
+                 col_idx=None, workspace=None, stream=None):
+    """Decoded lists without a plan (sift_decode_tiles): (row_ptr, col_idx)
+    device int32 tensors; workspace is allocated here when None."""
+    torch = _torch()
+    fn = "sift_decode_tiles"
+    dev = la.device if la is not None else ca.device
+    la_n, ca_n = bitmap_bytes(seg_offsets, prompt_seg_ptr, num_q_heads, tile)
+    require(fn, la, "local_bitmap", "uint8", la_n)
+    require(fn, ca, "cross_bitmap", "uint8", ca_n)
+    M = sum(-(-int(seg_offsets[s + 1] - seg_offsets[s]) // tile)
+            for s in range(len(seg_offsets) - 1))
+    cap = list_capacity(seg_offsets, prompt_seg_ptr, num_q_heads, tile)
+    if row_ptr is None:
+        row_ptr = torch.empty(num_q_heads * M + 1, dtype=torch.int32, device=dev)
+    if col_idx is None:
+        col_idx = torch.empty(max(1, cap), dtype=torch.int32, device=dev)
+    n = decode_workspace_bytes(seg_offsets, prompt_seg_ptr, num_q_heads, tile)
+    if workspace is None:
+        workspace = torch.empty(max(n, 1), dtype=torch.uint8, device=dev)
+    require(fn, row_ptr, "row_ptr", "int32", num_q_heads * M + 1, dev)
+    require(fn, col_idx, "col_idx", "int32", cap, dev)
+    require(fn, workspace, "workspace", "uint8", n, dev)
+    lay, keep = layout_struct(seg_offsets, prompt_seg_ptr)
+    check(fn, lib().sift_decode_tiles(ctypes.byref(lay), _ptr(la), _ptr(ca), tile, num_q_heads,
+                                      _ptr(row_ptr), _ptr(col_idx), col_idx.numel(),
+                                      _ptr(workspace), workspace.numel(), _stream_ptr(stream)))
+    return row_ptr, col_idx
 
 
 def extract_sizes(doc_offsets, num_q_heads, tile):

@@ -479,11 +479,13 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(KernArgs ka) {
 }
 
 // Merge the pieces of the split units.  Piece p left its normalised
-// output O_p (in the output's type), its reference max m_p (log2 domain) and
-// its row sum l_p, relative to 2^m_p.  With M the largest m_p among pieces
-// that saw keys and w_p = l_p 2^(m_p - M), a row's output is
-// sum w_p O_p / sum w_p.  Block (s, y) takes rows 32y .. 32y + 31 of split
-// unit s; thread t owns row 32y + t/8 and head dims 16 (t%8) .. + 15.
+// output O_p (fp32 output: fp32; bf16 output: a bf16 and the bf16 of its
+// rounding error, 16 significant bits together), its reference max m_p
+// (log2 domain) and its row sum l_p, relative to 2^m_p.  With M the largest
+// m_p among pieces that saw keys and w_p = l_p 2^(m_p - M), a row's output
+// is sum w_p O_p / sum w_p, rounded once to the output's type.  Block (s, y)
+// takes rows 32y .. 32y + 31 of split unit s; thread t owns row 32y + t/8
+// and head dims 16 (t%8) .. + 15.
 template <bool kOutF32>
 __global__ __launch_bounds__(256) void combine_kernel(PlanTables pt, WorkTables wt, AttnArgs a) {
   using OutT = typename std::conditional<kOutF32, float, __bf16>::type;
@@ -509,8 +511,9 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanTables pt, WorkTables 
 #pragma unroll
   for (int j = 0; j < kDims; ++j) acc[j] = 0.f;
   float wsum = 0.f;
-  const OutT* po = static_cast<const OutT*>(wt.part_o) +
-                   (static_cast<int64_t>(sp.y) * kUnitRows + prow) * kD + d0;
+  const int64_t pbase = (static_cast<int64_t>(sp.y) * kUnitRows + prow) * kD + d0;
+  const OutT* po = static_cast<const OutT*>(wt.part_o) + pbase;
+  const __bf16* plo = static_cast<const __bf16*>(wt.part_lo) + pbase;  // bf16 output only
 #pragma unroll 2
   for (int p = 0; p < sp.z; ++p) {
     const float2 x = ml[static_cast<int64_t>(p) * kUnitRows];
@@ -527,11 +530,15 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanTables pt, WorkTables 
         for (int e = 0; e < 4; ++e) acc[4 * c + e] += w * val[e];
       } else {
         const u32x4 raw = *reinterpret_cast<const u32x4*>(src + c * kVec);
+        const u32x4 rlo = *reinterpret_cast<const u32x4*>(plo + static_cast<int64_t>(p) *
+                                                                      kUnitRows * kD + c * kVec);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {  // bf16 -> f32 is exact: the high half of the word
-          const unsigned u = raw[e];
-          acc[8 * c + 2 * e] += w * __builtin_bit_cast(float, u << 16);
-          acc[8 * c + 2 * e + 1] += w * __builtin_bit_cast(float, u & 0xffff0000u);
+          const unsigned u = raw[e], l = rlo[e];
+          acc[8 * c + 2 * e] += w * (__builtin_bit_cast(float, u << 16) +
+                                     __builtin_bit_cast(float, l << 16));
+          acc[8 * c + 2 * e + 1] += w * (__builtin_bit_cast(float, u & 0xffff0000u) +
+                                         __builtin_bit_cast(float, l & 0xffff0000u));
         }
       }
     }

@@ -9,6 +9,7 @@
 #include <cstdint>
 #include <cstring>
 #include <limits>
+#include <mutex>
 #include <new>
 #include <numeric>
 #include <vector>
@@ -38,6 +39,7 @@ struct sift_plan {
   int32_t* row_ptr = nullptr;  // [num_rows + 1]
   int32_t* col_idx = nullptr;  // [list_capacity]
   bool steps_paged = false;    // the last decode wrote page-pool rows into the steps
+  hipStream_t last_stream = nullptr;  // the stream of the plan's last enqueued work
 };
 
 namespace {
@@ -339,12 +341,78 @@ const char* sift_status_string(int32_t status) {
 
 namespace {
 
+// Pinned host staging for stream-ordered uploads of plan tables.  A buffer
+// is handed out to one call at a time; after the call has enqueued its copy
+// it records an event, and the buffer is reused once that event has
+// completed (the copy has read it).  Buffers live until the process ends.
+struct StagingBuf {
+  int device;
+  void* host;
+  size_t cap;
+  hipEvent_t done;
+  bool taken;
+};
+std::mutex g_staging_mu;
+std::vector<StagingBuf> g_staging;
+
+// Index of a free pinned buffer of at least n bytes on the current device.
+sift_status staging_acquire(size_t n, size_t* idx) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return SIFT_E_HIP;
+  std::lock_guard<std::mutex> lock(g_staging_mu);
+  for (size_t i = 0; i < g_staging.size(); ++i) {
+    StagingBuf& b = g_staging[i];
+    if (b.taken || b.device != dev || b.cap < n) continue;
+    const hipError_t q = hipEventQuery(b.done);
+    if (q == hipErrorNotReady) continue;
+    if (q != hipSuccess) return SIFT_E_HIP;
+    b.taken = true;
+    *idx = i;
+    return SIFT_OK;
+  }
+  size_t cap = 1 << 16;
+  while (cap < n) cap <<= 1;
+  StagingBuf b{dev, nullptr, cap, nullptr, true};
+  if (hipHostMalloc(&b.host, cap, hipHostMallocDefault) != hipSuccess) return SIFT_E_HIP;
+  if (hipEventCreateWithFlags(&b.done, hipEventDisableTiming) != hipSuccess) {
+    (void)hipHostFree(b.host);
+    return SIFT_E_HIP;
+  }
+  g_staging.push_back(b);
+  *idx = g_staging.size() - 1;
+  return SIFT_OK;
+}
+
+// Hand a buffer back; with a stream, once the copies enqueued on it so far
+// are done.
+sift_status staging_release(size_t idx, hipStream_t stream, bool record) {
+  std::lock_guard<std::mutex> lock(g_staging_mu);
+  StagingBuf& b = g_staging[idx];
+  b.taken = false;
+  if (record && hipEventRecord(b.done, stream) != hipSuccess) return SIFT_E_HIP;
+  return SIFT_OK;
+}
+
+// How the plan's tables reach the device.
+enum class Upload {
+  kBlocking,   // hipMemcpy into the plan's own hipMalloc (sift_plan_create)
+  kStaged,     // hipMemcpyAsync on `stream` from pinned staging: no host wait
+  kPageable,   // hipMemcpyAsync on `stream` from host memory, then a wait for
+               // `stream` (no allocation at all)
+};
+
 // The plan's device memory: with ws == nullptr a hipMalloc of its own, else
-// the caller's workspace ws of ws_bytes (tables uploaded on `stream`, which
-// is waited for).  With bytes_only != nullptr only the size is computed.
+// ws (ws_bytes, 256-byte aligned): the caller's workspace, stream-ordered
+// scratch or static scratch, written on `stream` as `up` says.  With
+// bytes_only != nullptr only the size is computed.
+//
+// Layout: the tables, then the schedule's bucket sizes and the attention's
+// redo flag (zero: uploaded with the tables, and left so by every pass that
+// uses them), then the decode and merge scratch.
 sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t num_kv_heads,
                         int32_t head_dim, int32_t tile, void* ws, size_t ws_bytes,
-                        hipStream_t stream, size_t* bytes_only, sift_plan** plan_out) {
+                        hipStream_t stream, Upload up, size_t* bytes_only,
+                        sift_plan** plan_out) {
   if (layout == nullptr || (plan_out == nullptr && bytes_only == nullptr)) return SIFT_E_NULL;
   if (plan_out != nullptr) *plan_out = nullptr;
   if (num_q_heads < 1 || num_kv_heads < 1 || num_q_heads % num_kv_heads != 0) return SIFT_E_SHAPE;
@@ -375,6 +443,10 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   const size_t o_rec = put(blob, hp.rec);  // step counts and first steps: written by decode
   const size_t o_launch = put(blob, hp.launch);  // written by the schedule pass
   const size_t o_splits = put(blob, hp.splits);
+  // the schedule's bucket sizes, then the bf16 attention's redo flag and
+  // counter: zeros, uploaded with the tables
+  constexpr size_t kHistWords = sift::kNumXcd * sift::kSchedBuckets + 2;
+  const size_t o_hist = put(blob, std::vector<int32_t>(kHistWords, 0));
   const int64_t rows = static_cast<int64_t>(hp.num_tiles) * num_q_heads;
   const int64_t cap = hp.dense_tiles * num_q_heads;
   const int64_t U = static_cast<int64_t>(hp.unit_head.size());
@@ -390,13 +462,12 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   const int64_t step_cap = hp.step_off.empty() ? 0 : hp.step_off.back();
   const size_t o_sub = align(o_steps + (std::max<int64_t>(step_cap, 1) + 8) * 8);
   // per-step sub-tile masks, T < 64 only
-  const size_t o_hist = align(o_sub + (tile < 64 ? (std::max<int64_t>(step_cap, 1) + 8) * 4 : 0));
-  // the schedule's bucket sizes, then the bf16 attention's redo flag and
-  // counter: zero at creation, and left so by every pass that uses them
-  constexpr size_t kHistBytes = sift::kNumXcd * sift::kSchedBuckets * 4 + 2 * 4;
-  const size_t o_part_o = align(o_hist + kHistBytes);
+  const size_t o_part_o =
+      align(o_sub + (tile < 64 ? (std::max<int64_t>(step_cap, 1) + 8) * 4 : 0));
   const int64_t slot_rows = hp.part_slots * sift::kUnitRows;
-  const size_t o_part_ml = align(o_part_o + slot_rows * head_dim * 4);  // fp32 or bf16 output
+  // the pieces' outputs: fp32, or bf16 plus the bf16 of its rounding error
+  const size_t o_part_lo = align(o_part_o + slot_rows * head_dim * 4);
+  const size_t o_part_ml = align(o_part_lo + slot_rows * head_dim * 2);
   const size_t total = o_part_ml + std::max<int64_t>(slot_rows, 1) * 8;
 
   if (bytes_only != nullptr) {
@@ -421,25 +492,28 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   plan->dev_bytes = total;
   if (ws == nullptr) {
     if (hipMalloc(&plan->dev, total) != hipSuccess) return fail();
-    if (!blob.empty() &&
-        hipMemcpy(plan->dev, blob.data(), blob.size(), hipMemcpyHostToDevice) != hipSuccess)
-      return fail();
-    // the schedule's bucket sizes start at zero; each schedule pass leaves them so
-    if (hipMemset(static_cast<uint8_t*>(plan->dev) + o_hist, 0, kHistBytes) != hipSuccess)
+    if (hipMemcpy(plan->dev, blob.data(), blob.size(), hipMemcpyHostToDevice) != hipSuccess)
       return fail();
   } else {
-    // the caller's workspace, in stream order: the upload waits for earlier
-    // work on the stream (which may still read the workspace), and the host
-    // copy of the tables must outlive it
     plan->dev = ws;
     plan->owns_dev = false;
-    if (!blob.empty() && hipMemcpyAsync(plan->dev, blob.data(), blob.size(),
-                                        hipMemcpyHostToDevice, stream) != hipSuccess)
-      return fail();
-    if (hipMemsetAsync(static_cast<uint8_t*>(plan->dev) + o_hist, 0, kHistBytes, stream) !=
-        hipSuccess)
-      return fail();
-    if (hipStreamSynchronize(stream) != hipSuccess) return fail();
+    plan->last_stream = stream;
+    if (up == Upload::kStaged) {
+      // copy from pinned staging: the call returns without waiting, and the
+      // staging buffer is reused only after the copy has read it
+      size_t idx = 0;
+      if (staging_acquire(blob.size(), &idx) != SIFT_OK) return fail();
+      std::memcpy(g_staging[idx].host, blob.data(), blob.size());
+      const bool ok = hipMemcpyAsync(plan->dev, g_staging[idx].host, blob.size(),
+                                     hipMemcpyHostToDevice, stream) == hipSuccess;
+      if (staging_release(idx, stream, ok) != SIFT_OK || !ok) return fail();
+    } else {
+      // host memory: the blob must outlive the copy, so wait for the stream
+      if (hipMemcpyAsync(plan->dev, blob.data(), blob.size(), hipMemcpyHostToDevice,
+                         stream) != hipSuccess)
+        return fail();
+      if (hipStreamSynchronize(stream) != hipSuccess) return fail();
+    }
   }
   auto P = [plan](size_t off) {
     return reinterpret_cast<int32_t*>(static_cast<uint8_t*>(plan->dev) + off);
@@ -473,6 +547,7 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   plan->wt.sub = tile < 64 ? reinterpret_cast<uint32_t*>(P(o_sub)) : nullptr;
   plan->wt.splits = reinterpret_cast<const int4*>(P(o_splits));
   plan->wt.part_o = static_cast<void*>(P(o_part_o));
+  plan->wt.part_lo = static_cast<void*>(P(o_part_lo));
   plan->wt.part_ml = reinterpret_cast<float2*>(P(o_part_ml));
   plan->wt.redo = P(o_hist) + sift::kNumXcd * sift::kSchedBuckets;
   plan->wt.num_units = static_cast<int32_t>(U);
@@ -502,6 +577,32 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   return SIFT_OK;
 }
 
+// Arguments of the one-shot forms, checked on the host before anything is
+// enqueued; *need receives the scratch bytes of their plan.
+sift_status check_prefill(const sift_tensor* q, const sift_tensor* k, const sift_tensor* v,
+                          const sift_layout* layout, const uint8_t* la, const uint8_t* ca,
+                          int32_t tile, const sift_tensor* out, size_t* need) {
+  if (q == nullptr || k == nullptr || v == nullptr || out == nullptr || layout == nullptr)
+    return SIFT_E_NULL;
+  if (q->heads < 1 || k->heads < 1 || q->heads % k->heads != 0) return SIFT_E_SHAPE;
+  if (q->head_dim != 64 && q->head_dim != 128) return SIFT_E_UNSUPPORTED;
+  if (tile != 16 && tile != 32 && tile != 64 && tile != 128) return SIFT_E_UNSUPPORTED;
+  HostPlan hp;
+  sift_status st = build_host_plan(layout, q->heads, k->heads, tile, hp);
+  if (st != SIFT_OK) return st;
+  st = check_io(q, k, v, out, hp.num_tokens, q->heads, k->heads, q->head_dim, tile);
+  if (st != SIFT_OK) return st;
+  if (hp.la_bytes > 0 && la == nullptr) return SIFT_E_NULL;
+  if (hp.ca_bytes > 0 && ca == nullptr) return SIFT_E_NULL;
+  return create_plan(layout, q->heads, k->heads, q->head_dim, tile, nullptr, 0, nullptr,
+                     Upload::kBlocking, need, nullptr);
+}
+
+// Plans made only to decode lists: the lists do not depend on the kv heads
+// or the head size, so the smallest attention scratch is taken.
+constexpr int32_t kDecodeKvHeads = 1;
+constexpr int32_t kDecodeHeadDim = 64;
+
 }  // namespace
 
 extern "C" {
@@ -511,7 +612,7 @@ sift_status sift_plan_create(const sift_layout* layout, int32_t num_q_heads,
                              sift_plan** plan_out) {
   if (plan_out == nullptr) return SIFT_E_NULL;
   return create_plan(layout, num_q_heads, num_kv_heads, head_dim, tile, nullptr, 0, nullptr,
-                     nullptr, plan_out);
+                     Upload::kBlocking, nullptr, plan_out);
 }
 
 sift_status sift_workspace_bytes(const sift_layout* layout, int32_t num_q_heads,
@@ -519,14 +620,15 @@ sift_status sift_workspace_bytes(const sift_layout* layout, int32_t num_q_heads,
                                  size_t* bytes) {
   if (bytes == nullptr) return SIFT_E_NULL;
   return create_plan(layout, num_q_heads, num_kv_heads, head_dim, tile, nullptr, 0, nullptr,
-                     bytes, nullptr);
+                     Upload::kBlocking, bytes, nullptr);
 }
 
 sift_status sift_plan_destroy(sift_plan* plan) {
   if (plan == nullptr) return SIFT_OK;
   sift_status st = SIFT_OK;
   if (plan->dev != nullptr && plan->owns_dev) {
-    if (hipDeviceSynchronize() != hipSuccess) st = SIFT_E_HIP;
+    // the plan's last work may still read its memory
+    if (hipStreamSynchronize(plan->last_stream) != hipSuccess) st = SIFT_E_HIP;
     if (hipFree(plan->dev) != hipSuccess) st = SIFT_E_HIP;
   }
   delete plan;
@@ -539,9 +641,9 @@ sift_status sift_plan_get_info(const sift_plan* plan, sift_plan_info* info) {
   return SIFT_OK;
 }
 
-sift_status sift_decode_tiles(sift_plan* plan, const uint8_t* local_bitmap,
-                              const uint8_t* cross_bitmap, int32_t* row_ptr, int32_t* col_idx,
-                              int64_t col_capacity, void* stream) {
+sift_status sift_plan_decode_tiles(sift_plan* plan, const uint8_t* local_bitmap,
+                                   const uint8_t* cross_bitmap, int32_t* row_ptr,
+                                   int32_t* col_idx, int64_t col_capacity, void* stream) {
   if (plan == nullptr || row_ptr == nullptr) return SIFT_E_NULL;
   if (plan->info.la_bytes > 0 && local_bitmap == nullptr) return SIFT_E_NULL;
   if (plan->info.ca_bytes > 0 && cross_bitmap == nullptr) return SIFT_E_NULL;
@@ -555,14 +657,15 @@ sift_status sift_decode_tiles(sift_plan* plan, const uint8_t* local_bitmap,
                                            static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return SIFT_E_HIP;
   plan->steps_paged = false;
+  plan->last_stream = static_cast<hipStream_t>(stream);
   return SIFT_OK;
 }
 
 sift_status sift_plan_decode(sift_plan* plan, const uint8_t* local_bitmap,
                              const uint8_t* cross_bitmap, void* stream) {
   if (plan == nullptr) return SIFT_E_NULL;
-  return sift_decode_tiles(plan, local_bitmap, cross_bitmap, plan->row_ptr, plan->col_idx,
-                           plan->info.list_capacity, stream);
+  return sift_plan_decode_tiles(plan, local_bitmap, cross_bitmap, plan->row_ptr, plan->col_idx,
+                                plan->info.list_capacity, stream);
 }
 
 sift_status sift_sparse_attention(sift_plan* plan, const sift_tensor* q, const sift_tensor* k,
@@ -604,6 +707,7 @@ sift_status sift_sparse_attention(sift_plan* plan, const sift_tensor* q, const s
   } else {
     e = sift::launch_attn_f32(plan->pt, a, s);
   }
+  plan->last_stream = s;
   return e == hipSuccess ? SIFT_OK : SIFT_E_HIP;
 }
 
@@ -636,6 +740,7 @@ sift_status sift_plan_attention(sift_plan* plan, const sift_tensor* q, const sif
   const hipStream_t s = static_cast<hipStream_t>(stream);
   const hipError_t e = q->dtype == SIFT_BF16 ? sift::launch_attn_bf16(plan->pt, work(plan), a, s)
                                              : sift::launch_attn_f32(plan->pt, a, s);
+  plan->last_stream = s;
   return e == hipSuccess ? SIFT_OK : SIFT_E_HIP;
 }
 
@@ -687,6 +792,7 @@ sift_status sift_plan_run_paged(sift_plan* plan, const sift_tensor* q, const sif
   const hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = sift::launch_decode(plan->pt, work(plan), local_bitmap, cross_bitmap,
                                      plan->counts, plan->row_ptr, plan->col_idx, pages, s);
+  plan->last_stream = s;
   if (e != hipSuccess) return SIFT_E_HIP;
   plan->steps_paged = true;
   sift::AttnArgs a{};
@@ -706,6 +812,7 @@ sift_status sift_plan_run_paged(sift_plan* plan, const sift_tensor* q, const sif
   a.pages = pages;
   e = q->dtype == SIFT_BF16 ? sift::launch_attn_bf16(plan->pt, work(plan), a, s)
                             : sift::launch_attn_f32(plan->pt, a, s);
+  plan->last_stream = s;
   return e == hipSuccess ? SIFT_OK : SIFT_E_HIP;
 }
 
@@ -713,28 +820,21 @@ sift_status sift_sparse_prefill(const sift_tensor* q, const sift_tensor* k, cons
                                 const sift_layout* doc_offsets, const uint8_t* local_bitmap,
                                 const uint8_t* cross_bitmap, int32_t tile, sift_tensor* out,
                                 void* stream) {
-  if (q == nullptr || k == nullptr || v == nullptr || out == nullptr || doc_offsets == nullptr)
-    return SIFT_E_NULL;
-  // validate layout, shapes and bitmaps on the host before touching the device
-  {
-    if (q->heads < 1 || k->heads < 1 || q->heads % k->heads != 0) return SIFT_E_SHAPE;
-    if (q->head_dim != 64 && q->head_dim != 128) return SIFT_E_UNSUPPORTED;
-    if (tile != 16 && tile != 32 && tile != 64 && tile != 128) return SIFT_E_UNSUPPORTED;
-    HostPlan hp;
-    sift_status st0 = build_host_plan(doc_offsets, q->heads, k->heads, tile, hp);
-    if (st0 != SIFT_OK) return st0;
-    st0 = check_io(q, k, v, out, hp.num_tokens, q->heads, k->heads, q->head_dim, tile);
-    if (st0 != SIFT_OK) return st0;
-    if (hp.la_bytes > 0 && local_bitmap == nullptr) return SIFT_E_NULL;
-    if (hp.ca_bytes > 0 && cross_bitmap == nullptr) return SIFT_E_NULL;
-  }
-  sift_plan* plan = nullptr;
-  sift_status st = sift_plan_create(doc_offsets, q->heads, k->heads, q->head_dim, tile, &plan);
+  size_t need = 0;
+  sift_status st = check_prefill(q, k, v, doc_offsets, local_bitmap, cross_bitmap, tile, out,
+                                 &need);
   if (st != SIFT_OK) return st;
-  st = sift_plan_run(plan, q, k, v, local_bitmap, cross_bitmap, 0.f, out, stream);
-  if (st == SIFT_OK && hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess)
-    st = SIFT_E_HIP;
-  const sift_status st2 = sift_plan_destroy(plan);
+  // stream-ordered scratch: allocated, used and freed in the order of `stream`
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  void* ws = nullptr;
+  if (hipMallocAsync(&ws, need, s) != hipSuccess) return SIFT_E_HIP;
+  sift_plan* plan = nullptr;
+  st = create_plan(doc_offsets, q->heads, k->heads, q->head_dim, tile, ws, need, s,
+                   Upload::kStaged, nullptr, &plan);
+  if (st == SIFT_OK)
+    st = sift_plan_run(plan, q, k, v, local_bitmap, cross_bitmap, 0.f, out, stream);
+  const sift_status st2 = sift_plan_destroy(plan);  // host state only: ws is freed below
+  if (hipFreeAsync(ws, s) != hipSuccess && st == SIFT_OK) return SIFT_E_HIP;
   return st != SIFT_OK ? st : st2;
 }
 
@@ -743,34 +843,57 @@ sift_status sift_sparse_prefill_ex(const sift_tensor* q, const sift_tensor* k,
                                    const uint8_t* local_bitmap, const uint8_t* cross_bitmap,
                                    int32_t tile, float softmax_scale, void* workspace,
                                    size_t workspace_bytes, sift_tensor* out, void* stream) {
-  if (q == nullptr || k == nullptr || v == nullptr || out == nullptr || doc_offsets == nullptr)
-    return SIFT_E_NULL;
+  size_t need = 0;
+  sift_status st = check_prefill(q, k, v, doc_offsets, local_bitmap, cross_bitmap, tile, out,
+                                 &need);
+  if (st != SIFT_OK) return st;
   if (workspace == nullptr) return SIFT_E_NULL;
-  {
-    if (q->heads < 1 || k->heads < 1 || q->heads % k->heads != 0) return SIFT_E_SHAPE;
-    if (q->head_dim != 64 && q->head_dim != 128) return SIFT_E_UNSUPPORTED;
-    if (tile != 16 && tile != 32 && tile != 64 && tile != 128) return SIFT_E_UNSUPPORTED;
-    HostPlan hp;
-    sift_status st0 = build_host_plan(doc_offsets, q->heads, k->heads, tile, hp);
-    if (st0 != SIFT_OK) return st0;
-    st0 = check_io(q, k, v, out, hp.num_tokens, q->heads, k->heads, q->head_dim, tile);
-    if (st0 != SIFT_OK) return st0;
-    if (hp.la_bytes > 0 && local_bitmap == nullptr) return SIFT_E_NULL;
-    if (hp.ca_bytes > 0 && cross_bitmap == nullptr) return SIFT_E_NULL;
-    size_t need = 0;
-    st0 = create_plan(doc_offsets, q->heads, k->heads, q->head_dim, tile, nullptr, 0, nullptr,
-                      &need, nullptr);
-    if (st0 != SIFT_OK) return st0;
-    if (workspace_bytes < need) return SIFT_E_CAPACITY;
-    if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return SIFT_E_UNSUPPORTED;
-  }
-  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (workspace_bytes < need) return SIFT_E_CAPACITY;
+  if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return SIFT_E_UNSUPPORTED;
   sift_plan* plan = nullptr;
-  sift_status st = create_plan(doc_offsets, q->heads, k->heads, q->head_dim, tile, workspace,
-                               workspace_bytes, s, nullptr, &plan);
+  st = create_plan(doc_offsets, q->heads, k->heads, q->head_dim, tile, workspace,
+                   workspace_bytes, static_cast<hipStream_t>(stream), Upload::kStaged, nullptr,
+                   &plan);
   if (st != SIFT_OK) return st;
   st = sift_plan_run(plan, q, k, v, local_bitmap, cross_bitmap, softmax_scale, out, stream);
   const sift_status st2 = sift_plan_destroy(plan);  // host state only: the workspace is the caller's
+  return st != SIFT_OK ? st : st2;
+}
+
+sift_status sift_decode_workspace_bytes(const sift_layout* layout, int32_t num_q_heads,
+                                        int32_t tile, size_t* bytes) {
+  if (bytes == nullptr) return SIFT_E_NULL;
+  return create_plan(layout, num_q_heads, kDecodeKvHeads, kDecodeHeadDim, tile, nullptr, 0,
+                     nullptr, Upload::kBlocking, bytes, nullptr);
+}
+
+sift_status sift_decode_tiles(const sift_layout* layout, const uint8_t* local_bitmap,
+                              const uint8_t* cross_bitmap, int32_t tile, int32_t num_q_heads,
+                              int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
+                              void* workspace, size_t workspace_bytes, void* stream) {
+  if (layout == nullptr || row_ptr == nullptr || workspace == nullptr) return SIFT_E_NULL;
+  if (num_q_heads < 1) return SIFT_E_SHAPE;
+  if (tile != 16 && tile != 32 && tile != 64 && tile != 128) return SIFT_E_UNSUPPORTED;
+  HostPlan hp;
+  sift_status st = build_host_plan(layout, num_q_heads, kDecodeKvHeads, tile, hp);
+  if (st != SIFT_OK) return st;
+  if (hp.la_bytes > 0 && local_bitmap == nullptr) return SIFT_E_NULL;
+  if (hp.ca_bytes > 0 && cross_bitmap == nullptr) return SIFT_E_NULL;
+  const int64_t cap = hp.dense_tiles * num_q_heads;
+  if (cap > 0 && col_idx == nullptr) return SIFT_E_NULL;
+  if (col_capacity < cap) return SIFT_E_CAPACITY;
+  size_t need = 0;
+  if ((st = sift_decode_workspace_bytes(layout, num_q_heads, tile, &need)) != SIFT_OK) return st;
+  if (workspace_bytes < need) return SIFT_E_CAPACITY;
+  if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return SIFT_E_UNSUPPORTED;
+  sift_plan* plan = nullptr;
+  st = create_plan(layout, num_q_heads, kDecodeKvHeads, kDecodeHeadDim, tile, workspace,
+                   workspace_bytes, static_cast<hipStream_t>(stream), Upload::kStaged, nullptr,
+                   &plan);
+  if (st != SIFT_OK) return st;
+  st = sift_plan_decode_tiles(plan, local_bitmap, cross_bitmap, row_ptr, col_idx, col_capacity,
+                              stream);
+  const sift_status st2 = sift_plan_destroy(plan);  // host state only
   return st != SIFT_OK ? st : st2;
 }
 

@@ -127,6 +127,7 @@ struct WorkTables {
                               // unit's M-block k lists key tile s of the step (device scratch)
   const int4* splits;         // [NS] {record of the first piece, first slot, slots, 0}
   void* part_o;               // [slots][kUnitRows][head_dim], output type (device scratch)
+  void* part_lo;              // bf16 output: the same shape, part_o's bf16 rounding error
   float2* part_ml;            // [slots][kUnitRows] {reference max, row sum}
   int32_t* redo;              // [2] bf16 attention: {flag: do every unit again exactly,
                               // finished workgroups of that pass} (device scratch, zero

@@ -14,7 +14,7 @@ def test_library_loads_and_exports_every_declared_symbol():
     L = B.lib()
     names = B.header_functions()
     assert "sift_sparse_prefill" in names and "sift_decode_tiles" in names
-    assert len(names) == 16
+    assert len(names) == 18
     for n in names:
         assert hasattr(L, n), n
     # the binding declares every one of them too
@@ -153,3 +153,27 @@ def test_prefill_ex_rejects_workspace_and_arguments_on_the_host():
     assert _prefill_ex(q, k, k, [0, 64, 32, 160], ps, 1 << 20, n) == 3   # layout
     assert _prefill_ex(q, k, k, so, ps, 1 << 20, n, tile=48) == 4        # tile
     assert _prefill_ex(q, k, k, so, ps, 1 << 20, n, la=0) == 1           # bit vectors
+
+
+def test_layout_form_decode_checks_before_the_device():
+    """sift_decode_tiles (layout + bit vectors + caller workspace) refuses bad
+    arguments on the host, before anything is enqueued."""
+    so, ps = [0, 128, 256, 288], [0, 3]
+    lay, keep = B.layout_struct(so, ps)
+    n = ctypes.c_size_t()
+    assert B.lib().sift_decode_workspace_bytes(ctypes.byref(lay), 2, 16, ctypes.byref(n)) == 0
+    assert n.value > 0
+    cap = B.list_capacity(so, ps, 2, 16)
+    assert cap == 2 * (8 * 9 // 2 + (8 * 8 + 8 * 9 // 2) + (2 * 16 + 2 * 3 // 2))
+
+    def call(tile=16, ws=256, ws_bytes=None, col_cap=cap, la=1, ca=1):
+        return B.lib().sift_decode_tiles(ctypes.byref(lay), ctypes.c_void_p(la), ctypes.c_void_p(ca),
+                                         tile, 2, ctypes.c_void_p(1), ctypes.c_void_p(1), col_cap,
+                                         ctypes.c_void_p(ws), n.value if ws_bytes is None else ws_bytes,
+                                         None)
+    assert call(ws=0) == 1                       # no workspace
+    assert call(la=0) == 1                       # documents need their LA bits
+    assert call(tile=48) == 4
+    assert call(col_cap=cap - 1) == 5
+    assert call(ws_bytes=n.value - 1) == 5
+    assert call(ws=255) == 4                     # misaligned workspace

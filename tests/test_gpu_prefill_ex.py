@@ -78,3 +78,62 @@ def test_one_workspace_serves_consecutive_calls():
         torch.cuda.synchronize()
         assert torch.equal(o, r)
     say(f"[ex] one workspace of {need[0]} bytes, 3 calls: equal")
+
+
+@pytest.mark.parametrize("name,kw", [("tiny", {}), ("llama8b_4k", {}), ("custom16", {}),
+                                     ("custom128", {})])
+def test_layout_form_decode(name, kw):
+    """sift_decode_tiles (layout, bit vectors, tile, caller workspace; no
+    plan) gives the oracle's lists bit for bit, like the plan's decode."""
+    from gpu_helpers import oracle_csr
+    from paper_2606_09441_amd import decode_tiles
+    if name.startswith("custom"):
+        t = int(name[6:])
+        wl = W.custom([[300, 64, 129, 75], [5], [1, 64, 0]], tile=t, hq=4, hkv=2, d=64,
+                      dtype="f32", seed=t, p_la=0.4, p_ca=0.3)
+    else:
+        wl = W.make(name, **kw)
+    dev = device()
+    la = torch.from_numpy(wl.la if wl.la.size else np.zeros(1, np.uint8)).to(dev)
+    ca = torch.from_numpy(wl.ca if wl.ca.size else np.zeros(1, np.uint8)).to(dev)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        rp, ci = decode_tiles(wl.seg_offsets, wl.prompt_seg_ptr, la, ca, wl.hq, tile=wl.tile,
+                              stream=s)
+    s.synchronize()
+    rp = rp.cpu().numpy().astype(np.int64)
+    ci = ci[: int(rp[-1])].cpu().numpy().astype(np.int64)
+    erp, eci = oracle_csr(wl)
+    assert np.array_equal(rp, erp) and np.array_equal(ci, eci)
+    say(f"[ex] layout-form decode {wl.name} T={wl.tile}: nnz={ci.size} bit-exact")
+
+
+def test_one_shot_forms_are_stream_ordered():
+    """The one-shot forms enqueue everything on the caller's stream: on a
+    side stream, several calls queued back to back without a wait (the
+    stream-ordered scratch of sift_sparse_prefill, one workspace for
+    sift_sparse_prefill_ex) give the plan run's outputs."""
+    from paper_2606_09441_amd import Plan, sparse_prefill, sparse_prefill_ex, workspace_bytes
+    wl = W.custom([[256, 192, 100], [64, 64, 64]], tile=64, hq=4, hkv=1, d=128, dtype="bf16",
+                  seed=5)
+    q, k, v, la, ca = _dev(wl)
+    with Plan(wl.seg_offsets, wl.prompt_seg_ptr, 4, 1, 128, 64) as plan:
+        ref = plan.run(q, k, v, la, ca)
+        torch.cuda.synchronize()
+    n = workspace_bytes(wl.seg_offsets, wl.prompt_seg_ptr, 4, 1, 128, 64)
+    ws = torch.empty(n, dtype=torch.uint8, device=q.device)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    outs = []
+    with torch.cuda.stream(s):
+        for i in range(6):
+            if i % 2:
+                outs.append(sparse_prefill_ex(q, k, v, wl.seg_offsets, wl.prompt_seg_ptr, la, ca,
+                                              tile=64, workspace=ws, stream=s))
+            else:
+                outs.append(sparse_prefill(q, k, v, wl.seg_offsets, wl.prompt_seg_ptr, la, ca,
+                                           tile=64, stream=s))
+    s.synchronize()
+    for o in outs:
+        assert torch.equal(o, ref)
+    say("[ex] 6 one-shot calls queued on a side stream: equal to the plan run")
