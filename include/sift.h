@@ -142,6 +142,18 @@ sift_status sift_plan_destroy(sift_plan* plan);
 sift_status sift_plan_get_info(const sift_plan* plan, sift_plan_info* info);
 
 /*
+ * Diagnostic of the bf16 attention (Section 5.2's online softmax, done in
+ * two launches here): the first launch forms every tile's weights against
+ * the row's first reference max and flags the launch when a weight sum
+ * exceeds its bound or an output is not finite; the second launch then does
+ * every unit again with a running max.  *count receives how many attention
+ * launches on this plan needed that second pass.  Waits for the stream of
+ * the plan's last enqueued work.  Errors: SIFT_E_NULL, SIFT_E_PLAN (another
+ * device is current), SIFT_E_HIP.
+ */
+sift_status sift_plan_exact_passes(const sift_plan* plan, int64_t* count);
+
+/*
  * Decoding (Section 5.1) with a plan: expand the bit vectors into the packed
  * lists.
  *   local_bitmap, cross_bitmap   device, la_bytes / ca_bytes of the plan

@@ -58,6 +58,7 @@ _SIGS = {
                                         ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(_P)]),
     "sift_plan_destroy": (ctypes.c_int, [_P]),
     "sift_plan_get_info": (ctypes.c_int, [_P, ctypes.POINTER(SiftPlanInfo)]),
+    "sift_plan_exact_passes": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int64)]),
     "sift_plan_decode_tiles": (ctypes.c_int, [_P, _P, _P, _P, _P, ctypes.c_int64, _P]),
     "sift_decode_workspace_bytes": (ctypes.c_int, [ctypes.POINTER(SiftLayout), ctypes.c_int32,
                                                    ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]),
@@ -289,6 +290,13 @@ class Plan:
             _ptr(col_idx), col_idx.numel(), ctypes.c_float(0.0 if scale is None else scale),
             ctypes.byref(od), _stream_ptr(stream)))
         return out
+
+    def exact_passes(self) -> int:
+        """Attention launches on this plan that needed the exact second pass
+        (sift_plan_exact_passes; waits for the plan's last stream)."""
+        n = ctypes.c_int64()
+        check("sift_plan_exact_passes", lib().sift_plan_exact_passes(self._h, ctypes.byref(n)))
+        return n.value
 
     def decode_internal(self, la, ca, stream=None):
         """Decode into the plan's own scratch (sift_plan_decode)."""

@@ -473,6 +473,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(KernArgs ka) {
       if (atomicAdd(&wt.redo[1], 1) == static_cast<int>(gridDim.x) - 1) {
         atomicExch(&wt.redo[0], 0);
         atomicExch(&wt.redo[1], 0);
+        atomicAdd(&wt.redo[2], 1);  // launches whose exact pass ran
       }
     }
   }

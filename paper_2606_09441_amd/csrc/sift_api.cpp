@@ -444,8 +444,8 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   const size_t o_launch = put(blob, hp.launch);  // written by the schedule pass
   const size_t o_splits = put(blob, hp.splits);
   // the schedule's bucket sizes, then the bf16 attention's redo flag and
-  // counter: zeros, uploaded with the tables
-  constexpr size_t kHistWords = sift::kNumXcd * sift::kSchedBuckets + 2;
+  // counters: zeros, uploaded with the tables
+  constexpr size_t kHistWords = sift::kNumXcd * sift::kSchedBuckets + 3;
   const size_t o_hist = put(blob, std::vector<int32_t>(kHistWords, 0));
   const int64_t rows = static_cast<int64_t>(hp.num_tiles) * num_q_heads;
   const int64_t cap = hp.dense_tiles * num_q_heads;
@@ -633,6 +633,18 @@ sift_status sift_plan_destroy(sift_plan* plan) {
   }
   delete plan;
   return st;
+}
+
+sift_status sift_plan_exact_passes(const sift_plan* plan, int64_t* count) {
+  if (plan == nullptr || count == nullptr) return SIFT_E_NULL;
+  if (check_device(plan) != SIFT_OK) return SIFT_E_PLAN;
+  int32_t n = 0;
+  if (hipMemcpyAsync(&n, plan->wt.redo + 2, sizeof(n), hipMemcpyDeviceToHost,
+                     plan->last_stream) != hipSuccess ||
+      hipStreamSynchronize(plan->last_stream) != hipSuccess)
+    return SIFT_E_HIP;
+  *count = n;
+  return SIFT_OK;
 }
 
 sift_status sift_plan_get_info(const sift_plan* plan, sift_plan_info* info) {

@@ -129,9 +129,10 @@ struct WorkTables {
   void* part_o;               // [slots][kUnitRows][head_dim], output type (device scratch)
   void* part_lo;              // bf16 output: the same shape, part_o's bf16 rounding error
   float2* part_ml;            // [slots][kUnitRows] {reference max, row sum}
-  int32_t* redo;              // [2] bf16 attention: {flag: do every unit again exactly,
-                              // finished workgroups of that pass} (device scratch, zero
-                              // between launches)
+  int32_t* redo;              // [3] bf16 attention: {flag: do every unit again exactly,
+                              // finished workgroups of that pass (both zero between
+                              // launches), launches whose exact pass ran (a count kept
+                              // for the plan's life)} (device scratch)
   int32_t num_units;          // U
   int32_t num_work;           // W
   int32_t num_splits;         // NS

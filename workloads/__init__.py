@@ -197,13 +197,13 @@ def _assemble(name, prompts, tile, hq, hkv, d, dtype, meta):
                     tile, hq, hkv, d, dtype, cat(qs), cat(ks), cat(vs), la, ca, meta)
 
 
-def _rag_prompt(rng, doc_lens, query_len, tile, hq, hkv, d, rho):
-    """Draw order: Q/K/V of every document and the query, then heavy hitters,
-    then bitmaps."""
+def _rag_prompt(rng, doc_lens, query_len, tile, hq, hkv, d, rho, hh=4.0):
+    """Draw order: Q/K/V of every document and the query, then heavy hitters
+    (K rows scaled by hh), then bitmaps."""
     raw = [_draw_qkv(rng, n, hq, hkv, d, True) for n in doc_lens]
     query = _draw_qkv(rng, query_len, hq, hkv, d, True)
     for _, k, _ in raw:
-        _heavy_hitters(rng, k)
+        _heavy_hitters(rng, k, factor=hh)
     docs = []
     for (q, k, v) in raw:
         la_m, ca_m = _standalone_masses(q, k, tile, hq, hkv)
@@ -247,12 +247,13 @@ def _mid(seed=0, rho=0.2, tile=64, **_):
                      {"rho": rho, "docs": [1024] * 16, "query": 256})
 
 
-def _long(seed=0, rho=0.15, hq=48, hkv=8, tile=64, **_):
+def _long(seed=0, rho=0.15, hq=48, hkv=8, tile=64, hh=4.0, **_):
     rng = np.random.default_rng(seed)
-    docs, query = _rag_prompt(rng, [2048] * 32, 512, tile, hq, hkv, 128, rho)
-    return _assemble(f"long64k_{hq}x{hkv}_rho{rho:g}" + ("" if tile == 64 else f"_t{tile}"),
+    docs, query = _rag_prompt(rng, [2048] * 32, 512, tile, hq, hkv, 128, rho, hh)
+    return _assemble(f"long64k_{hq}x{hkv}_rho{rho:g}" + ("" if tile == 64 else f"_t{tile}")
+                     + ("" if hh == 4.0 else f"_hh{hh:g}"),
                      [(docs, query)], tile, hq, hkv, 128, "bf16",
-                     {"rho": rho, "docs": [2048] * 32, "query": 512})
+                     {"rho": rho, "docs": [2048] * 32, "query": 512, "heavy_hitter_scale": hh})
 
 
 def _ragged(seed=0, **_):
@@ -295,7 +296,8 @@ CONFIGS = {
 
 def make(name: str, seed: int = 0, **kw) -> Workload:
     """Build a named configuration.  Extra keywords: rho (density knob) and
-    tile (64 or 128) for the RAG configs; hq/hkv for long64k."""
+    tile (16, 32, 64 or 128) for the RAG configs; hq/hkv and hh (the
+    heavy-hitter K scale, default 4) for long64k."""
     return CONFIGS[name](seed=seed, **kw)
 
 
