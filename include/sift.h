@@ -325,6 +325,34 @@ sift_status sift_sparse_prefill_ex(const sift_tensor* q, const sift_tensor* k,
                                    size_t workspace_bytes, sift_tensor* out, void* stream);
 
 /*
+ * For callers that cannot allocate device memory (code under stream capture,
+ * tight serving loops, harnesses that forbid hipMalloc): the computation of
+ * sift_sparse_prefill_ex with the library's own static device scratch in
+ * place of the caller's workspace.  Nothing is allocated on the device and
+ * no hipMalloc, hipFree or allocating library routine is called.
+ *   Arguments as in sift_sparse_prefill_ex, without the workspace.
+ *   The scratch is sift_static_scratch_bytes() = 256 MiB per GPU, held from
+ *   the library's load on that GPU until the process ends; a layout whose
+ *   plan needs more (sift_workspace_bytes) is refused with SIFT_E_CAPACITY
+ *   before anything is enqueued.
+ *   The plan's tables are copied from host memory on `stream`, and the call
+ *   waits for `stream` once that copy is enqueued (so that the host copy
+ *   can be freed); decode and attention are then enqueued and the call
+ *   returns without waiting for them.
+ *   Every call on one GPU uses the same scratch, which keeps the last call's
+ *   contents: calls that overlap on one GPU (other streams, other threads)
+ *   race and give wrong results.  Order them.
+ * Errors: as sift_sparse_prefill_ex, with SIFT_E_CAPACITY for a layout that
+ *   does not fit the scratch.
+ */
+sift_status sift_sparse_prefill_static(const sift_tensor* q, const sift_tensor* k,
+                                       const sift_tensor* v, const sift_layout* doc_offsets,
+                                       const uint8_t* local_bitmap,
+                                       const uint8_t* cross_bitmap, int32_t tile,
+                                       float softmax_scale, sift_tensor* out, void* stream);
+size_t sift_static_scratch_bytes(void);
+
+/*
  * Offline metadata extraction (Sections 4.1, 4.2; made by a dense
  * standalone prefill of each document, Section 4.4).
  *

@@ -88,6 +88,13 @@ _SIGS = {
                                               ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftLayout),
                                               _P, _P, ctypes.c_int32, ctypes.c_float, _P,
                                               ctypes.c_size_t, ctypes.POINTER(SiftTensor), _P]),
+    "sift_sparse_prefill_static": (ctypes.c_int, [ctypes.POINTER(SiftTensor),
+                                                  ctypes.POINTER(SiftTensor),
+                                                  ctypes.POINTER(SiftTensor),
+                                                  ctypes.POINTER(SiftLayout), _P, _P,
+                                                  ctypes.c_int32, ctypes.c_float,
+                                                  ctypes.POINTER(SiftTensor), _P]),
+    "sift_static_scratch_bytes": (ctypes.c_size_t, []),
     "sift_rope": (ctypes.c_int, [ctypes.POINTER(SiftTensor), ctypes.POINTER(SiftTensor), _P, _P, _P]),
     "sift_extract_sizes": (ctypes.c_int, [ctypes.c_int32, _P, ctypes.c_int32, ctypes.c_int32,
                                           ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t),
@@ -399,6 +406,29 @@ def sparse_prefill_ex(q, k, v, seg_offsets, prompt_seg_ptr, la, ca, tile=64, sca
         tile, ctypes.c_float(0.0 if scale is None else scale), _ptr(workspace),
         workspace.numel() * workspace.element_size(), ctypes.byref(od), _stream_ptr(stream)))
     return out
+
+
+def sparse_prefill_static(q, k, v, seg_offsets, prompt_seg_ptr, la, ca, tile=64, scale=None,
+                          out=None, stream=None):
+    """The one-shot form on the library's static device scratch
+    (sift_sparse_prefill_static): nothing is allocated on the device; calls
+    on one GPU must not overlap."""
+    torch = _torch()
+    _check_bits("sift_sparse_prefill_static", q, la, ca, seg_offsets, prompt_seg_ptr, tile)
+    if out is None:
+        out = torch.empty_like(q)
+    lay, keep = layout_struct(seg_offsets, prompt_seg_ptr)
+    qd, kd, vd, od = tensor_desc(q), tensor_desc(k), tensor_desc(v), tensor_desc(out)
+    check("sift_sparse_prefill_static", lib().sift_sparse_prefill_static(
+        ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), ctypes.byref(lay), _ptr(la), _ptr(ca),
+        tile, ctypes.c_float(0.0 if scale is None else scale), ctypes.byref(od),
+        _stream_ptr(stream)))
+    return out
+
+
+def static_scratch_bytes() -> int:
+    """Bytes of the static scratch of sparse_prefill_static (per GPU)."""
+    return int(lib().sift_static_scratch_bytes())
 
 
 def decode_workspace_bytes(seg_offsets, prompt_seg_ptr, num_q_heads, tile=64):

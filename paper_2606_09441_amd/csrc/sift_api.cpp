@@ -598,6 +598,30 @@ sift_status check_prefill(const sift_tensor* q, const sift_tensor* k, const sift
                      Upload::kBlocking, need, nullptr);
 }
 
+// Scratch for sift_sparse_prefill_static: one array per GPU, held from the
+// library's load on that GPU until the process ends.  Host code never uses
+// the array's name as an address: each device's address is taken once with
+// hipGetSymbolAddress, with that device current, and kept here.
+constexpr size_t kStaticScratchBytes = size_t(256) << 20;
+__device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+constexpr int kMaxDevices = 64;
+std::once_flag g_scratch_once[kMaxDevices];
+void* g_scratch_ptr[kMaxDevices] = {};
+hipError_t g_scratch_err[kMaxDevices] = {};
+
+// The current device's address of the scratch array.
+sift_status static_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return SIFT_E_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return SIFT_E_UNSUPPORTED;
+  std::call_once(g_scratch_once[dev], [dev]() {
+    g_scratch_err[dev] = hipGetSymbolAddress(&g_scratch_ptr[dev], HIP_SYMBOL(scratch));
+  });
+  if (g_scratch_err[dev] != hipSuccess || g_scratch_ptr[dev] == nullptr) return SIFT_E_HIP;
+  *out = g_scratch_ptr[dev];
+  return SIFT_OK;
+}
+
 // Plans made only to decode lists: the lists do not depend on the kv heads
 // or the head size, so the smallest attention scratch is taken.
 constexpr int32_t kDecodeKvHeads = 1;
@@ -908,5 +932,30 @@ sift_status sift_decode_tiles(const sift_layout* layout, const uint8_t* local_bi
   const sift_status st2 = sift_plan_destroy(plan);  // host state only
   return st != SIFT_OK ? st : st2;
 }
+
+sift_status sift_sparse_prefill_static(const sift_tensor* q, const sift_tensor* k,
+                                       const sift_tensor* v, const sift_layout* doc_offsets,
+                                       const uint8_t* local_bitmap, const uint8_t* cross_bitmap,
+                                       int32_t tile, float softmax_scale, sift_tensor* out,
+                                       void* stream) {
+  size_t need = 0;
+  sift_status st = check_prefill(q, k, v, doc_offsets, local_bitmap, cross_bitmap, tile, out,
+                                 &need);
+  if (st != SIFT_OK) return st;
+  if (need > kStaticScratchBytes) return SIFT_E_CAPACITY;
+  void* ws = nullptr;
+  if ((st = static_scratch(&ws)) != SIFT_OK) return st;
+  // tables from host memory: the call waits for the copy, so nothing is
+  // allocated to hold them
+  sift_plan* plan = nullptr;
+  st = create_plan(doc_offsets, q->heads, k->heads, q->head_dim, tile, ws, kStaticScratchBytes,
+                   static_cast<hipStream_t>(stream), Upload::kPageable, nullptr, &plan);
+  if (st != SIFT_OK) return st;
+  st = sift_plan_run(plan, q, k, v, local_bitmap, cross_bitmap, softmax_scale, out, stream);
+  const sift_status st2 = sift_plan_destroy(plan);  // host state only
+  return st != SIFT_OK ? st : st2;
+}
+
+size_t sift_static_scratch_bytes(void) { return kStaticScratchBytes; }
 
 }  // extern "C"

@@ -14,7 +14,7 @@ def test_library_loads_and_exports_every_declared_symbol():
     L = B.lib()
     names = B.header_functions()
     assert "sift_sparse_prefill" in names and "sift_decode_tiles" in names
-    assert len(names) == 19
+    assert len(names) == 21
     for n in names:
         assert hasattr(L, n), n
     # the binding declares every one of them too
