@@ -3,25 +3,28 @@
 // packed, ascending int32 list of key tiles per (query head, M-block).
 //
 // Three kernels:
-//   decode_count  one thread per row (h, m): number of tiles the row lists.
-//                 Document rows: popcount of LA bits i(i+1)/2 .. i(i+1)/2+i-1
-//                 (row i of the lower triangle, diagonal excluded) + 1 for the
-//                 always-computed diagonal + popcount of the CA vector of
-//                 every earlier document of the prompt.  Query rows: every
+//   decode_count  one workgroup per (query head, segment): each row's number
+//                 of listed tiles.  Document rows: popcount of LA bits
+//                 i(i+1)/2 .. i(i+1)/2+i-1 (row i of the lower triangle,
+//                 diagonal excluded) + 1 for the always-computed diagonal +
+//                 the popcount of the CA vectors of the earlier documents of
+//                 the prompt (one sum per workgroup).  Query rows: every
 //                 tile of the prompt up to the row's own (Section 5.1: query
-//                 M-blocks count all causal N-blocks).
-//   decode_scan   exclusive prefix sum of the counts -> row_ptr (one
-//                 workgroup, coalesced two-pass scan).
-//   decode_write  one wavefront per attention work unit (query head, up to
-//                 four consecutive M-blocks of one segment): CA pages of the
-//                 earlier documents in document order, then the LA tiles
-//                 (diagonals included); each chunk of 64 candidate tiles
-//                 becomes indices through a ballot and a lane-prefix
-//                 popcount, so every output is dense and in ascending global
-//                 tile order.  It writes every row's list and the unit's
-//                 merged step list (the union of the rows' lists, each step
-//                 flagged with the M-blocks that list it), which the
-//                 attention kernel streams.
+//                 M-blocks count all causal N-blocks), in closed form.  The
+//                 counts are scanned inside the (head, segment); the last
+//                 workgroup scans the (head, segment) totals: the "designated
+//                 offsets" of Section 5.1 are their sum.
+//   decode_write  one wavefront per attention list unit (query head, up to
+//                 eight consecutive M-blocks of one segment): writes its
+//                 rows' row_ptr, then the CA pages of the earlier documents
+//                 in document order, then the LA tiles (diagonals included);
+//                 each chunk of 64 candidate tiles becomes indices through a
+//                 ballot and a lane-prefix popcount, so every output is dense
+//                 and in ascending global tile order.  It writes every row's
+//                 list and the unit's merged step list (the union of the
+//                 rows' lists, each step flagged with the M-blocks that list
+//                 it), which the attention kernel streams.
+//   schedule_scatter  the launch order of the attention's work units.
 // Bits are most significant first inside each byte (Section 4.1).
 
 #include "sift_internal.h"
@@ -51,77 +54,100 @@ __device__ int popc_bits(const uint8_t* v, int b0, int n) {
   return c;
 }
 
-__global__ __launch_bounds__(256) void decode_count(PlanTables pt, const uint8_t* __restrict__ la,
-                                                    const uint8_t* __restrict__ ca,
-                                                    int32_t* __restrict__ counts) {
-  const int64_t M = pt.num_tiles;
-  const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (r >= M * pt.num_q_heads) return;
-  const int h = static_cast<int>(r / M);
-  const int m = static_cast<int>(r - static_cast<int64_t>(h) * M);
-  const int s = pt.tile_seg[m];
-  if (pt.seg_kind[s] == kQuery) {
-    counts[r] = m - pt.tile_lo[m] + 1;
-    return;
+// Inclusive scan of v over the 256 threads of a block (wavefront scans,
+// then the four wavefront totals through LDS); returns the block total.
+__device__ __forceinline__ int32_t block_scan256(int32_t v, int32_t& incl, int32_t* wtot) {
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  int32_t x = v;
+  for (int off = 1; off < 64; off <<= 1) {
+    const int32_t y = __shfl_up(x, off, 64);
+    if (lane >= off) x += y;
   }
-  const int i = m - pt.seg_tile0[s];
-  const int P = pt.seg_pages[s];
-  const uint8_t* lav = la + pt.seg_la_off[s] + static_cast<int64_t>(h) * la_nbytes(P);
-  int c = 1 + popc_bits(lav, i * (i + 1) / 2, i);
-  for (int e = pt.seg_first[s]; e < s; ++e) {
-    const int Pe = pt.seg_pages[e];
-    c += popc_bits(ca + pt.seg_ca_off[e] + static_cast<int64_t>(h) * ca_nbytes(Pe), 0, Pe);
+  if (lane == 63) wtot[w] = x;
+  __syncthreads();
+  int32_t before = 0, total = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    before += j < w ? wtot[j] : 0;
+    total += wtot[j];
   }
-  counts[r] = c;
+  __syncthreads();  // wtot is reused by the next call
+  incl = before + x;
+  return total;
 }
 
-// Exclusive scan of n counts into row_ptr[0..n]; a single 1024-thread block.
-// Thread t owns a contiguous chunk; chunk totals are scanned with wavefront
-// shuffles and one LDS step across the 16 wavefronts.
-// Exclusive prefix sum of the counts in one workgroup of 16 wavefronts.
-// Wavefront w owns a chunk of consecutive rows (a multiple of 256 long).
-// Pass 1 sums the chunk with coalesced loads; the chunk offsets come from the
-// 16 totals in LDS.  Pass 2 walks the chunk 256 rows at a time, 4 per lane:
-// a lane-local prefix, a wavefront scan of the lane sums, coalesced stores.
-__global__ __launch_bounds__(1024) void decode_scan(const int32_t* __restrict__ counts,
-                                                    int32_t* __restrict__ row_ptr, int64_t n) {
-  __shared__ int32_t wsum[16];
+// Block b = h S + s: the rows of segment s for query head h.  A document row
+// i lists the marked pages of the earlier documents of its prompt, the
+// marked tiles j < i of its LA row and its diagonal; a query row lists every
+// tile of its prompt up to its own (Section 5.1).  Each row's count goes to
+// local[] as its offset inside the (head, segment); the total to seg_base[b].
+// The last block to finish turns seg_base into each (head, segment)'s first
+// list entry (the rows' order is h-major, then tile order) and writes
+// row_ptr[Hq M] = nnz.
+__global__ __launch_bounds__(256) void decode_count(PlanTables pt, WorkTables wt,
+                                                    const uint8_t* __restrict__ la,
+                                                    const uint8_t* __restrict__ ca,
+                                                    int32_t* __restrict__ local,
+                                                    int32_t* __restrict__ row_ptr) {
+  __shared__ int32_t wtot[4];
+  __shared__ int last;
+  const int S = pt.num_segments;
+  const int b = blockIdx.x;
+  const int h = b / S, s = b - h * S;
   const int t = threadIdx.x;
-  const int lane = t & 63;
-  const int w = t >> 6;
-  const int64_t per = ((n + 15) / 16 + 255) / 256 * 256;
-  const int64_t a = min(n, static_cast<int64_t>(w) * per);
-  const int64_t z = min(n, a + per);
-  int32_t s = 0;
-  for (int64_t i = a + lane; i < z; i += 64) s += counts[i];
-  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
-  if (lane == 0) wsum[w] = s;
-  __syncthreads();
-  int32_t base = 0;
-  for (int j = 0; j < w; ++j) base += wsum[j];
-  for (int64_t g = a; g < z; g += 256) {
-    const int64_t i0 = g + 4 * lane;
-    int32_t v[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) v[k] = i0 + k < z ? counts[i0 + k] : 0;
-    const int32_t own = v[0] + v[1] + v[2] + v[3];
-    int32_t x = own;  // inclusive scan of the lane sums
-    for (int off = 1; off < 64; off <<= 1) {
-      const int32_t y = __shfl_up(x, off, 64);
-      if (lane >= off) x += y;
+  const int P = pt.seg_pages[s];
+  const int tile0 = pt.seg_tile0[s];
+  int32_t* lrow = local + static_cast<int64_t>(h) * pt.num_tiles + tile0;
+  int32_t total;
+  if (pt.seg_kind[s] == kQuery) {
+    // row i lists a + i tiles, a = the tiles before the segment plus one
+    const int a = tile0 - pt.seg_tile0[pt.seg_first[s]] + 1;
+    for (int i = t; i < P; i += 256) lrow[i] = i * a + i * (i - 1) / 2;
+    total = P * a + P * (P - 1) / 2;
+  } else {
+    // marked pages of the earlier documents: the same for every row
+    int32_t c = 0;
+    for (int e = pt.seg_first[s] + t; e < s; e += 256) {
+      const int Pe = pt.seg_pages[e];
+      c += popc_bits(ca + pt.seg_ca_off[e] + static_cast<int64_t>(h) * ca_nbytes(Pe), 0, Pe);
     }
-    int32_t e = base + x - own;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      if (i0 + k < z) row_ptr[i0 + k] = e;
-      e += v[k];
+    int32_t dummy;
+    const int32_t cross = block_scan256(c, dummy, wtot);
+    const uint8_t* lav = la + pt.seg_la_off[s] + static_cast<int64_t>(h) * la_nbytes(P);
+    int32_t run = 0;
+    for (int i0 = 0; i0 < P; i0 += 256) {
+      const int i = i0 + t;
+      // the LA bits of row i before its diagonal, plus the diagonal itself
+      const int32_t cnt = i < P ? cross + 1 + popc_bits(lav, i * (i + 1) / 2, i) : 0;
+      int32_t incl;
+      const int32_t chunk = block_scan256(cnt, incl, wtot);
+      if (i < P) lrow[i] = run + incl - cnt;
+      run += chunk;
     }
-    base += __shfl(x, 63, 64);
+    total = run;
   }
   if (t == 0) {
-    int32_t total = 0;
-    for (int j = 0; j < 16; ++j) total += wsum[j];
-    row_ptr[n] = total;
+    wt.seg_base[b] = total;
+    __threadfence();
+    last = atomicAdd(wt.decode_done, 1) == static_cast<int>(gridDim.x) - 1;
+  }
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  const int n = gridDim.x;
+  int32_t run = 0;
+  for (int i0 = 0; i0 < n; i0 += 256) {
+    const int i = i0 + t;
+    const int32_t v =
+        i < n ? __hip_atomic_load(&wt.seg_base[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
+    int32_t incl;
+    const int32_t chunk = block_scan256(v, incl, wtot);
+    if (i < n) wt.seg_base[i] = run + incl - v;
+    run += chunk;
+  }
+  if (t == 0) {
+    row_ptr[static_cast<int64_t>(pt.num_q_heads) * pt.num_tiles] = run;
+    *wt.decode_done = 0;
   }
 }
 
@@ -243,7 +269,8 @@ template <int kNb, bool kGrouped, bool kHalves>
 __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt,
                                                     const uint8_t* __restrict__ la,
                                                     const uint8_t* __restrict__ ca,
-                                                    const int32_t* __restrict__ row_ptr,
+                                                    const int32_t* __restrict__ local,
+                                                    int32_t* __restrict__ row_ptr,
                                                     int32_t* __restrict__ col, KvPages pages) {
   const int lane = threadIdx.x & 63;
   const int u = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -258,8 +285,13 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   e.steps = wt.steps;
   e.pt = &pt;
   e.pages = pages;
+  const int s = pt.tile_seg[m0];
+  const int32_t base = wt.seg_base[h * pt.num_segments + s];
 #pragma unroll
-  for (int k = 0; k < kNb; ++k) e.pos[k] = k < nb ? row_ptr[r0 + k] : 0;
+  for (int k = 0; k < kNb; ++k) {
+    e.pos[k] = k < nb ? base + local[r0 + k] : 0;
+    if (k < nb && lane == 0) row_ptr[r0 + k] = e.pos[k];
+  }
   e.ps = wt.lu_off[u];
   e.wt = &wt;
   e.base = e.ps;
@@ -269,7 +301,6 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   e.m0 = m0;
   e.nb = nb;
   e.below = (1ull << lane) - 1ull;
-  const int s = pt.tile_seg[m0];
   const int mlast = m0 + nb - 1;
   constexpr bool grouped = kGrouped;
   if (pt.seg_kind[s] == kQuery && !grouped) {
@@ -520,32 +551,26 @@ hipError_t launch_schedule(const WorkTables& wt, hipStream_t stream) {
 hipError_t launch_decode(const PlanTables& pt, const WorkTables& wt, const uint8_t* la,
                          const uint8_t* ca, int32_t* counts, int32_t* row_ptr, int32_t* col_idx,
                          const KvPages& pages, hipStream_t stream) {
-  const int64_t rows = static_cast<int64_t>(pt.num_tiles) * pt.num_q_heads;
-  if (rows == 0) {  // empty layout: the scan alone writes row_ptr[0] = 0
-    hipLaunchKernelGGL(decode_scan, dim3(1), dim3(1024), 0, stream, counts, row_ptr, rows);
-    return hipGetLastError();
-  }
-  hipLaunchKernelGGL(decode_count, dim3(static_cast<unsigned>((rows + 255) / 256)), dim3(256), 0,
-                     stream, pt, la, ca, counts);
+  // one count block per (head, segment); the last one also writes row_ptr[Hq M]
+  const int64_t blocks = static_cast<int64_t>(pt.num_q_heads) * pt.num_segments;
+  hipLaunchKernelGGL(decode_count, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, pt,
+                     wt, la, ca, counts, row_ptr);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(decode_scan, dim3(1), dim3(1024), 0, stream, counts, row_ptr, rows);
-  e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (wt.num_units == 0) return hipSuccess;
   const dim3 wgrid(static_cast<unsigned>((wt.num_units + 3) / 4));
   if (pt.group == 4)
     hipLaunchKernelGGL((decode_write<8, true, false>), wgrid, dim3(256), 0, stream, pt, wt, la, ca,
-                       row_ptr, col_idx, pages);
+                       counts, row_ptr, col_idx, pages);
   else if (pt.group == 2)
     hipLaunchKernelGGL((decode_write<4, true, false>), wgrid, dim3(256), 0, stream, pt, wt, la, ca,
-                       row_ptr, col_idx, pages);
+                       counts, row_ptr, col_idx, pages);
   else if (pt.halves == 2)
     hipLaunchKernelGGL((decode_write<2, false, true>), wgrid, dim3(256), 0, stream, pt, wt, la, ca,
-                       row_ptr, col_idx, pages);
+                       counts, row_ptr, col_idx, pages);
   else
     hipLaunchKernelGGL((decode_write<2, false, false>), wgrid, dim3(256), 0, stream, pt, wt, la, ca,
-                       row_ptr, col_idx, pages);
+                       counts, row_ptr, col_idx, pages);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_schedule(wt, stream);

@@ -443,16 +443,18 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   const size_t o_rec = put(blob, hp.rec);  // step counts and first steps: written by decode
   const size_t o_launch = put(blob, hp.launch);  // written by the schedule pass
   const size_t o_splits = put(blob, hp.splits);
-  // the schedule's bucket sizes, then the bf16 attention's redo flag and
-  // counters: zeros, uploaded with the tables
-  constexpr size_t kHistWords = sift::kNumXcd * sift::kSchedBuckets + 3;
+  // the schedule's bucket sizes, the bf16 attention's redo flag and
+  // counters, the decode's finished-block count: zeros, uploaded with the
+  // tables
+  constexpr size_t kHistWords = sift::kNumXcd * sift::kSchedBuckets + 4;
   const size_t o_hist = put(blob, std::vector<int32_t>(kHistWords, 0));
   const int64_t rows = static_cast<int64_t>(hp.num_tiles) * num_q_heads;
   const int64_t cap = hp.dense_tiles * num_q_heads;
   const int64_t U = static_cast<int64_t>(hp.unit_head.size());
   auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
   const size_t o_counts = align(blob.size());
-  const size_t o_rowptr = align(o_counts + rows * 4);
+  const size_t o_segbase = align(o_counts + rows * 4);
+  const size_t o_rowptr = align(o_segbase + static_cast<int64_t>(hp.num_segments) * num_q_heads * 4);
   const size_t o_col = align(o_rowptr + (rows + 1) * 4);
   const int64_t W = static_cast<int64_t>(hp.wk_head.size());
   const size_t o_steps = align(o_col + std::max<int64_t>(cap, 1) * 4);
@@ -532,6 +534,7 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   plan->pt.halves = tile == 128 ? 2 : 1;
   plan->pt.group = tile < 64 ? 64 / tile : 1;
   plan->pt.num_tiles = hp.num_tiles;
+  plan->pt.num_segments = hp.num_segments;
   plan->pt.num_q_heads = num_q_heads;
   plan->wt.rec = reinterpret_cast<sift::WorkRec*>(P(o_rec));
   plan->wt.launch = reinterpret_cast<sift::WorkRec*>(P(o_launch));
@@ -550,6 +553,8 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   plan->wt.part_lo = static_cast<void*>(P(o_part_lo));
   plan->wt.part_ml = reinterpret_cast<float2*>(P(o_part_ml));
   plan->wt.redo = P(o_hist) + sift::kNumXcd * sift::kSchedBuckets;
+  plan->wt.decode_done = plan->wt.redo + 3;
+  plan->wt.seg_base = P(o_segbase);
   plan->wt.num_units = static_cast<int32_t>(U);
   plan->wt.num_work = static_cast<int32_t>(W);
   plan->wt.num_splits = static_cast<int32_t>(hp.splits.size() / 4);

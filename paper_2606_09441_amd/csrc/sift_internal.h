@@ -25,6 +25,7 @@ struct PlanTables {
   const int32_t* tile_len;    // tokens in tile m (T, or less for a last tile)
   const int32_t* tile_lo;     // first tile of m's prompt
   int32_t num_tiles;          // M
+  int32_t num_segments;       // S
   int32_t num_q_heads;        // Hq
   int32_t tile;               // T
   int32_t halves;             // T = 128: 2 (each tile is two 64-row/64-key halves); else 1
@@ -129,6 +130,10 @@ struct WorkTables {
   void* part_o;               // [slots][kUnitRows][head_dim], output type (device scratch)
   void* part_lo;              // bf16 output: the same shape, part_o's bf16 rounding error
   float2* part_ml;            // [slots][kUnitRows] {reference max, row sum}
+  int32_t* seg_base;          // [Hq * S] decode: each (head, segment)'s rows' list total,
+                              // then their first list entry (device scratch)
+  int32_t* decode_done;       // decode: finished count blocks (device scratch, zero between
+                              // decodes)
   int32_t* redo;              // [3] bf16 attention: {flag: do every unit again exactly,
                               // finished workgroups of that pass (both zero between
                               // launches), launches whose exact pass ran (a count kept
@@ -198,8 +203,10 @@ __device__ __forceinline__ TileSteps tile_steps(const PlanTables& pt, const KvPa
   return t;
 }
 
-// Decode (Section 5.1): count, scan, write.  The write pass runs per unit and
-// emits its M-blocks' lists and the unit's merged step list.
+// Decode (Section 5.1): count, write, schedule.  The count pass writes each
+// row's count as its offset inside its (head, segment) and scans the segment
+// totals; the write pass runs per unit, writes its rows' row_ptr, its
+// M-blocks' lists and the unit's merged step list.
 hipError_t launch_decode(const PlanTables& pt, const WorkTables& wt, const uint8_t* la,
                          const uint8_t* ca, int32_t* counts, int32_t* row_ptr, int32_t* col_idx,
                          const KvPages& pages, hipStream_t stream);
