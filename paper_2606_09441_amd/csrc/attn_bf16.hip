@@ -45,10 +45,11 @@
 //    VALU work does not overlap the MFMAs (the exponentials do), so every
 //    VALU instruction per step counts.  The first launch takes no row max
 //    per tile: a row's reference is the max of the first tile it sees, and
-//    later tiles' weights are checked by their sums (kSumMax).  If a check
-//    fails anywhere, or an output comes out non-finite, the launch raises a
-//    flag and the second launch does every unit again with a lazy running
-//    max (kLazy); otherwise the second launch returns at once.  P is rounded
+//    later tiles' weights are formed against it at whatever magnitude.  If
+//    an output or row sum comes out non-finite (a weight overflowed), the
+//    launch raises a flag and the second launch does every unit again with
+//    a lazy running max (kLazy); otherwise the second launch only merges
+//    the pieces of split units.  P is rounded
 //    to bf16 and the row sum adds exactly those rounded values
 //    (v_dot2_f32_bf16 against 1.0), so normalisation matches the weights
 //    the MFMA used.
@@ -89,19 +90,18 @@ constexpr int kBufferWord3 = 0x00020000;  // gfx9-family raw buffer resource wor
 constexpr float kLazy = 8.0f;
 
 // The pass over all units does not take a tile's row max at all.  A row's
-// reference max is the max of the first tile that gives it a key; later
-// tiles' weights P = 2^(s c - mref) are formed against it and bounded by
-// their sums: while a lane's share of a tile's sum (32 weights) is <=
-// kSumMax, every P is finite and <= kSumMax (bf16 P keeps its relative
-// precision at any magnitude, and l stays below 2^80).  When some share
-// exceeds it (a score more than 55 log2 units above the reference, or an
-// exp2 overflow), or O or l ends up infinite or NaN (|v| beyond about 2^50
-// with such weights, or non-finite inputs), the launch is flagged and a
-// second launch does every unit again with the lazy reference above
-// (kLazy), whose weights are <= 2^kLazy.  Neither happens with scores of
-// the usual range.
-constexpr float kSumMax = 0x1p60f;
-
+// reference max is the max of the first tile that gives it a key (that key's
+// weight is 1); later tiles' weights P = 2^(s c - mref) are formed against
+// it.  P rounded to bf16 keeps its relative precision at any magnitude
+// (bf16 has fp32's exponent range), and l and O accumulate in fp32, so the
+// result does not depend on the reference as long as nothing overflows:
+// weights far below the reference are negligible next to the reference's
+// own weight 1 in any case.  A weight, row sum or output beyond fp32's range
+// (scores more than about 120 log2 units above the row's first tile, |v|
+// large enough with such weights, or non-finite inputs) ends up infinite or
+// NaN in the row sum or the output, which the epilogue tests; the launch is
+// then flagged and a second launch does every unit again with the lazy
+// reference above (kLazy), whose weights are <= 2^kLazy.
 // Workgroups of the launch that does the units again (it returns at once
 // when the first launch raised no flag).
 constexpr int kRedoGrid = 512;
@@ -369,12 +369,16 @@ __device__ __forceinline__ void softmax_exp(const f32x16& s0, const f32x16& s1, 
 }
 
 // Rows without a reference take the row max of the next tile (scores s0,
-// s1) before its weights are formed.
+// s1) before its weights are formed.  Such a row has seen no key, so its O
+// and l are still 0 and nothing needs rescaling; rows that have a reference
+// keep it.
 template <int kG>
 __device__ __forceinline__ void first_ref(RowState& rs, const f32x16& s0, const f32x16& s1,
                                           float c) {
-  if (__builtin_amdgcn_ballot_w64(rs.mref == -INFINITY))
-    rescale<kG, false>(rs, tile_max(s0, s1) * c);
+  if (__builtin_amdgcn_ballot_w64(rs.mref == -INFINITY)) {
+    const float mx = tile_max(s0, s1) * c;
+    rs.mref = rs.mref == -INFINITY ? mx : rs.mref;
+  }
 }
 
 __device__ __forceinline__ void pv_tile(const PvArgs& v, int slot_off, const bf16x8 (&pb)[4],
@@ -439,46 +443,6 @@ struct KernArgs {
   AttnArgs a;
 };
 
-// kRedo = false: the first pass; workgroup b takes the unit of launch slot
-// b and flags the launch (wt.redo[0]) if a weight check fails.  kRedo =
-// true: the exact pass; when the flag is set, kRedoGrid workgroups do every
-// unit again, then the last one to finish clears the flag for the next
-// launch; otherwise they return at once.
-template <bool kOutF32, int kG, bool kRedo>
-__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(KernArgs ka) {
-  const PlanTables& pt = ka.pt;
-  const WorkTables& wt = ka.wt;
-  const AttnArgs& a = ka.a;
-  // K slot 0, K slot 1, V slot 0, V slot 1 (16 KB each)
-  __shared__ __attribute__((aligned(1024))) __bf16 smem[4 * kTile];
-  // the unit's partial-result slot, parked in LDS for the epilogue so that
-  // no register is held across the main loop (every wavefront writes the
-  // same value and reads back its own write)
-  __shared__ int slot_park;
-
-  if constexpr (!kRedo) {
-    const int4* __restrict__ rp = reinterpret_cast<const int4*>(wt.launch + blockIdx.x);
-#include "attn_bf16_unit.inc"
-  } else {
-    if (__hip_atomic_load(&wt.redo[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) return;
-    for (int u = blockIdx.x; u < wt.grid; u += gridDim.x) {
-      auto unit = [&](const int4* __restrict__ rp) {
-#include "attn_bf16_unit.inc"
-      };
-      unit(reinterpret_cast<const int4*>(wt.launch + u));
-      __syncthreads();  // LDS (slots, slot_park) is reused by the next unit
-    }
-    if (threadIdx.x == 0) {
-      __threadfence();
-      if (atomicAdd(&wt.redo[1], 1) == static_cast<int>(gridDim.x) - 1) {
-        atomicExch(&wt.redo[0], 0);
-        atomicExch(&wt.redo[1], 0);
-        atomicAdd(&wt.redo[2], 1);  // launches whose exact pass ran
-      }
-    }
-  }
-}
-
 // Merge the pieces of the split units.  Piece p left its normalised
 // output O_p (fp32 output: fp32; bf16 output: a bf16 and the bf16 of its
 // rounding error, 16 significant bits together), its reference max m_p
@@ -486,15 +450,15 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(KernArgs ka) {
 // m_p among pieces that saw keys and w_p = l_p 2^(m_p - M), a row's output
 // is sum w_p O_p / sum w_p, rounded once to the output's type.  Block (s, y)
 // takes rows 32y .. 32y + 31 of split unit s; thread t owns row 32y + t/8
-// and head dims 16 (t%8) .. + 15.
+// and head dims 16 (t%8) .. + 15.  Job j = 4 s + y.
 template <bool kOutF32>
-__global__ __launch_bounds__(256) void combine_kernel(PlanTables pt, WorkTables wt, AttnArgs a) {
+__device__ __forceinline__ void combine_job(const WorkTables& wt, const AttnArgs& a, int job) {
   using OutT = typename std::conditional<kOutF32, float, __bf16>::type;
   constexpr int kDims = 16;                         // per thread
   constexpr int kVec = 16 / sizeof(OutT);           // elements per 16-byte load
-  const int4 sp = wt.splits[blockIdx.x];  // {record of the first piece, first slot, slots}
+  const int4 sp = wt.splits[job >> 2];  // {record of the first piece, first slot, slots}
   const WorkRec* __restrict__ rp = wt.rec + sp.x;
-  const int row = blockIdx.y * 32 + (threadIdx.x >> 3);
+  const int row = (job & 3) * 32 + (threadIdx.x >> 3);
   const int d0 = (threadIdx.x & 7) * kDims;
   const int blk = row >> 6;
   const int r = row & 63;
@@ -564,6 +528,60 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanTables pt, WorkTables 
   }
 }
 
+// kRedo = false: the first pass; workgroup b takes the unit of launch slot
+// b and flags the launch (wt.redo[0]) if a weight check fails.  kRedo =
+// true: the exact pass; when the flag is set, kRedoGrid workgroups do every
+// unit again, then the last one to finish clears the flag for the next
+// launch; otherwise they return at once.
+template <bool kOutF32, int kG, bool kRedo>
+__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(KernArgs ka) {
+  const PlanTables& pt = ka.pt;
+  const WorkTables& wt = ka.wt;
+  const AttnArgs& a = ka.a;
+  // K slot 0, K slot 1, V slot 0, V slot 1 (16 KB each)
+  __shared__ __attribute__((aligned(1024))) __bf16 smem[4 * kTile];
+  // the unit's partial-result slot, parked in LDS for the epilogue so that
+  // no register is held across the main loop (every wavefront writes the
+  // same value and reads back its own write)
+  __shared__ int slot_park;
+
+  if constexpr (!kRedo) {
+    const int4* __restrict__ rp = reinterpret_cast<const int4*>(wt.launch + blockIdx.x);
+#include "attn_bf16_unit.inc"
+  } else {
+    constexpr int kJobs = kUnitRows / 32;  // merge jobs per split unit
+    const int jobs = wt.num_splits * kJobs;
+    if (__hip_atomic_load(&wt.redo[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
+      // the first pass stands: merge the pieces of the split units
+      for (int j = blockIdx.x; j < jobs; j += gridDim.x) combine_job<kOutF32>(wt, a, j);
+      return;
+    }
+    for (int u = blockIdx.x; u < wt.grid; u += gridDim.x) {
+      auto unit = [&](const int4* __restrict__ rp) {
+#include "attn_bf16_unit.inc"
+      };
+      unit(reinterpret_cast<const int4*>(wt.launch + u));
+      __syncthreads();  // LDS (slots, slot_park) is reused by the next unit
+    }
+    if (threadIdx.x == 0) {
+      __threadfence();
+      slot_park = atomicAdd(&wt.redo[1], 1) == static_cast<int>(gridDim.x) - 1;
+    }
+    __syncthreads();
+    if (slot_park) {
+      // the last workgroup: every piece is written; merge them all, then
+      // clear the flag for the next launch
+      __threadfence();
+      for (int j = 0; j < jobs; ++j) combine_job<kOutF32>(wt, a, j);
+      if (threadIdx.x == 0) {
+        atomicExch(&wt.redo[0], 0);
+        atomicExch(&wt.redo[1], 0);
+        atomicAdd(&wt.redo[2], 1);  // launches whose exact pass ran
+      }
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_attn_bf16(const PlanTables& pt, const WorkTables& wt, const AttnArgs& a,
@@ -597,13 +615,7 @@ hipError_t launch_attn_bf16(const PlanTables& pt, const WorkTables& wt, const At
   else
     e = g == 4 ? launch(std::false_type{}, I4{})
                : g == 2 ? launch(std::false_type{}, I2{}) : launch(std::false_type{}, I1{});
-  if (e != hipSuccess || wt.num_splits == 0) return e;
-  if (a.out_f32)
-    hipLaunchKernelGGL(combine_kernel<true>, dim3(wt.num_splits, kUnitRows / 32), dim3(256), 0,
-                       stream, pt, wt, a);
-  else
-    hipLaunchKernelGGL(combine_kernel<false>, dim3(wt.num_splits, kUnitRows / 32), dim3(256), 0,
-                       stream, pt, wt, a);
+  if (e != hipSuccess) return e;
   return hipGetLastError();
 }
 

@@ -2,12 +2,12 @@
 
 Section 5.2 keeps the online softmax of dense attention.  The bf16 kernel
 forms a tile's weights against the reference max a row took from its first
-tile and bounds them by their sums; a unit in which some sum exceeds the
-bound (a score far above the reference, or an exp2 overflow) is done again
-with the reference following every tile's max.  Here K rows are scaled up
-along each segment, so that later tiles score 2^30 to 2^200 times the first
-one: every unit fails the check and is redone.  The outputs must still
-match the fp64 oracle, for every tile variant and for split query units."""
+tile, at whatever magnitude; when a weight, row sum or output overflows
+fp32, the launch is done again with the reference following every tile's
+max.  Here K rows are scaled up along each segment, so that later tiles
+score up to 2^100 (finite weights) or far beyond 2^128 (overflow) times the
+first one.  The outputs must still match the fp64 oracle, for every tile
+variant and for split query units."""
 
 import numpy as np
 import pytest
@@ -48,8 +48,11 @@ def _parity(wl, tag):
 
 
 @pytest.mark.parametrize("tile", [16, 32, 64, 128])
-@pytest.mark.parametrize("top", [30.0, 80.0])
+@pytest.mark.parametrize("top", [15.0, 30.0, 80.0])
 def test_rising_scores_ragged_layouts(tile, top):
+    """top 15: weights up to about 2^100 times a row's first tile, still
+    finite, kept by the first pass; 30 and 80: some overflow, the exact pass
+    redoes the launch."""
     wl = _rising(W.custom(RAGGED, tile=tile, hq=4, hkv=2, d=128, dtype="bf16", seed=tile + 5,
                           p_la=0.5, p_ca=0.4), top)
     _parity(wl, f"T={tile} K x1..{top:g}")
@@ -122,3 +125,24 @@ def test_huge_values_with_rising_scores():
     say(f"[range] V ~ 2^100, K x1..10: max-abs / 2^100 {err:.3e}")
     assert np.isfinite(out).all()
     assert err <= BF16_TOL
+
+
+def test_large_finite_weights_need_no_second_pass():
+    """Scores rising by up to about 2^80 over a row's first tile: every weight
+    is finite, so the first pass keeps its result (no exact pass) and it
+    matches the oracle."""
+    from gpu_helpers import DevWorkload
+    wl = _rising(W.custom(RAGGED, tile=64, hq=4, hkv=2, d=128, dtype="bf16", seed=14,
+                          p_la=0.5, p_ca=0.4), 12.0)
+    dw = DevWorkload(wl)
+    try:
+        before = dw.plan.exact_passes()
+        out = dw.run().float().cpu().numpy()
+        ran = dw.plan.exact_passes() - before
+    finally:
+        dw.close()
+    ref = O.attention(oracle_layout(wl), wl.q, wl.k, wl.v, wl.la, wl.ca)
+    err = max_abs(out, ref)
+    say(f"[range] K x1..12: max-abs {err:.3e}, exact passes {ran}")
+    assert np.isfinite(out).all() and err <= BF16_TOL
+    assert ran == 0
