@@ -39,17 +39,24 @@ __device__ __forceinline__ int get_bit(const uint8_t* v, int b) {
   return (v[b >> 3] >> (7 - (b & 7))) & 1;
 }
 
-// Set bits among bits b0 .. b0+n-1 of v (MSB-first numbering).
+// Set bits among bits b0 .. b0+n-1 of v (MSB-first numbering).  The bytes
+// are read four at a time, their loads issued together.
 __device__ int popc_bits(const uint8_t* v, int b0, int n) {
-  int c = 0;
-  int b = b0;
+  if (n <= 0) return 0;
   const int end = b0 + n;
-  while (b < end) {
-    const int bit = b & 7;
-    const int take = min(8 - bit, end - b);
-    const unsigned mask = (0xFFu >> bit) & (0xFFu << (8 - bit - take));
-    c += __popc(static_cast<unsigned>(v[b >> 3]) & mask);
-    b += take;
+  const int last = (end - 1) >> 3;
+  int c = 0;
+  for (int w = b0 >> 3; w <= last; w += 4) {
+    unsigned byte[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) byte[q] = w + q <= last ? v[w + q] : 0u;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int lo = (w + q) * 8;  // bit number of the byte's most significant bit
+      const int a = max(b0 - lo, 0), z = min(end - lo, 8);
+      const unsigned m = a < z ? (0xFFu >> a) & (0xFFu << (8 - z)) : 0u;
+      c += __popc(byte[q] & m);
+    }
   }
   return c;
 }
@@ -105,26 +112,29 @@ __global__ __launch_bounds__(256) void decode_count(PlanTables pt, WorkTables wt
     for (int i = t; i < P; i += 256) lrow[i] = i * a + i * (i - 1) / 2;
     total = P * a + P * (P - 1) / 2;
   } else {
-    // marked pages of the earlier documents: the same for every row
+    // marked pages of the earlier documents (the same for every row) and
+    // the LA bits of each row before its diagonal: all loads issued first
+    const uint8_t* lav = la + pt.seg_la_off[s] + static_cast<int64_t>(h) * la_nbytes(P);
     int32_t c = 0;
     for (int e = pt.seg_first[s] + t; e < s; e += 256) {
       const int Pe = pt.seg_pages[e];
       c += popc_bits(ca + pt.seg_ca_off[e] + static_cast<int64_t>(h) * ca_nbytes(Pe), 0, Pe);
     }
-    int32_t dummy;
-    const int32_t cross = block_scan256(c, dummy, wtot);
-    const uint8_t* lav = la + pt.seg_la_off[s] + static_cast<int64_t>(h) * la_nbytes(P);
-    int32_t run = 0;
-    for (int i0 = 0; i0 < P; i0 += 256) {
+    int32_t own = t < P ? 1 + popc_bits(lav, t * (t + 1) / 2, t) : 0;  // rows 0..255
+    // one pass: the CA sum and the scan of the first 256 rows together
+    int32_t incl, cincl;
+    const int32_t first = block_scan256(own, incl, wtot);
+    const int32_t cross = block_scan256(c, cincl, wtot);
+    if (t < P) lrow[t] = incl - own + t * cross;
+    int32_t run = first;
+    for (int i0 = 256; i0 < P; i0 += 256) {  // longer documents: more rows
       const int i = i0 + t;
-      // the LA bits of row i before its diagonal, plus the diagonal itself
-      const int32_t cnt = i < P ? cross + 1 + popc_bits(lav, i * (i + 1) / 2, i) : 0;
-      int32_t incl;
+      const int32_t cnt = i < P ? 1 + popc_bits(lav, i * (i + 1) / 2, i) : 0;
       const int32_t chunk = block_scan256(cnt, incl, wtot);
-      if (i < P) lrow[i] = run + incl - cnt;
+      if (i < P) lrow[i] = run + incl - cnt + i * cross;
       run += chunk;
     }
-    total = run;
+    total = run + P * cross;
   }
   if (t == 0) {
     wt.seg_base[b] = total;
@@ -134,19 +144,39 @@ __global__ __launch_bounds__(256) void decode_count(PlanTables pt, WorkTables wt
   __syncthreads();
   if (!last) return;
   __threadfence();
+  // thread t takes the consecutive totals [t per, (t + 1) per): a serial
+  // sum, one block scan of the thread sums, then each thread's offsets
   const int n = gridDim.x;
-  int32_t run = 0;
-  for (int i0 = 0; i0 < n; i0 += 256) {
-    const int i = i0 + t;
-    const int32_t v =
-        i < n ? __hip_atomic_load(&wt.seg_base[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
-    int32_t incl;
-    const int32_t chunk = block_scan256(v, incl, wtot);
-    if (i < n) wt.seg_base[i] = run + incl - v;
-    run += chunk;
+  const int per = (n + 255) / 256;
+  const int a = min(n, t * per), z = min(n, a + per);
+  auto load8 = [&](int i0, int32_t (&v)[8]) {  // eight loads issued together
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+      v[q] = i0 + q < z ? __hip_atomic_load(&wt.seg_base[i0 + q], __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT)
+                        : 0;
+  };
+  int32_t sum = 0;
+  for (int i0 = a; i0 < z; i0 += 8) {
+    int32_t v[8];
+    load8(i0, v);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) sum += v[q];
+  }
+  int32_t incl;
+  const int32_t all = block_scan256(sum, incl, wtot);
+  int32_t run = incl - sum;
+  for (int i0 = a; i0 < z; i0 += 8) {
+    int32_t v[8];
+    load8(i0, v);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      if (i0 + q < z) wt.seg_base[i0 + q] = run;
+      run += v[q];
+    }
   }
   if (t == 0) {
-    row_ptr[static_cast<int64_t>(pt.num_q_heads) * pt.num_tiles] = run;
+    row_ptr[static_cast<int64_t>(pt.num_q_heads) * pt.num_tiles] = all;
     *wt.decode_done = 0;
   }
 }
@@ -185,17 +215,18 @@ struct Emitter {
     }
   }
 
-  __device__ __forceinline__ void emit(unsigned listed, int32_t n) {
+  // The same with the tile's first K/V row and length already loaded.
+  __device__ __forceinline__ void emit_at(unsigned listed, int32_t n, int32_t row0, int32_t len) {
     lists(listed, n);
     if constexpr (!kHalves) {
       // T = 64: one step per listed tile, in lane order
       const unsigned long long mu = __ballot(listed != 0u);
       if (listed != 0u) {
         const unsigned diag = (n >= m0 && n < m0 + nb) ? 1u << (n - m0) : 0u;
-        const int info = pt->tile_len[n] | static_cast<int>(listed << kStepListedShift) |
+        const int info = len | static_cast<int>(listed << kStepListedShift) |
                          static_cast<int>(diag << kStepDiagShift);
         const int32_t idx = ps + __popcll(mu & below);
-        const int2 st = make_int2(kv_row0(*pt, pages, n), info);
+        const int2 st = make_int2(row0, info);
         steps[idx] = st;
         if (whole && idx - base < kFirstSteps) wt->rec[w0].first[idx - base] = st;
       }
@@ -203,7 +234,7 @@ struct Emitter {
       return;
     }
     // one or two steps per listed tile, in lane order
-    const TileSteps ts = tile_steps(*pt, pages, n, listed, m0, nb);
+    const TileSteps ts = tile_steps_at(*pt, n, listed, m0, nb, row0, len);
     const unsigned long long mu1 = __ballot(ts.cnt >= 1), mu2 = __ballot(ts.cnt >= 2);
     const int32_t idx = ps + __popcll(mu1 & below) + __popcll(mu2 & below);
     for (int q = 0; q < ts.cnt; ++q) {
@@ -303,17 +334,64 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   e.below = (1ull << lane) - 1ull;
   const int mlast = m0 + nb - 1;
   constexpr bool grouped = kGrouped;
-  if (pt.seg_kind[s] == kQuery && !grouped) {
-    // every tile of the prompt up to the M-block (Section 5.1): M-block m0 +
-    // k lists n when n <= m0 + k
+  if constexpr (!grouped) {
+    // T >= 64: the candidates are the prompt's tiles lo .. mlast in order
+    // (the earlier documents' pages, then this segment's tiles), 64 per
+    // round; each round's loads are issued one round ahead.
+    //   query unit: M-block m0 + k lists n when n <= m0 + k (Section 5.1);
+    //   document unit: every M-block lists the CA-marked pages of the earlier
+    //   documents, and row r = i + k its LA-marked tiles j < r and j == r.
+    const bool query = pt.seg_kind[s] == kQuery;
     const int lo = pt.tile_lo[m0];
-    for (int k0 = lo; k0 <= mlast; k0 += 64) {
-      const int n = k0 + lane;
+    const int sd0 = pt.seg_tile0[s];
+    const int i = m0 - sd0;
+    const uint8_t* lav =
+        query ? la : la + pt.seg_la_off[s] + static_cast<int64_t>(h) * la_nbytes(pt.seg_pages[s]);
+    struct Cand {
+      int4 ti;
+      int32_t row0;
+      unsigned bits;  // the CA byte (earlier documents) or the LA bits per M-block
+    };
+    auto fetch = [&](int n) {
+      Cand c{make_int4(0, 0, -1, 0), 0, 0u};
+      if (n <= mlast) {
+        c.ti = pt.tile_info[n];
+        c.row0 = pages.table == nullptr ? c.ti.x : kv_row0(pt, pages, n);
+        if (!query) {
+          if (n < sd0) {
+            c.bits = ca[c.ti.z + static_cast<int64_t>(h) * (c.ti.w >> 3)];
+          } else {
+            const int j = n - sd0;
+#pragma unroll
+            for (int k = 0; k < kNb; ++k) {
+              const int r = i + k;
+              if (k < nb && j < r) c.bits |= static_cast<unsigned>(get_bit(lav, r * (r + 1) / 2 + j)) << k;
+            }
+          }
+        }
+      }
+      return c;
+    };
+    Cand cur = fetch(lo + lane);
+    for (int n0 = lo; n0 <= mlast; n0 += 64) {
+      const int n = n0 + lane;
+      const Cand nxt = fetch(n + 64);
       unsigned listed = 0u;
-      if (n <= mlast) listed = n < m0 ? all : (all & ~((1u << (n - m0)) - 1u));
-      e.emit(listed, n);
+      if (n <= mlast) {
+        if (query) {
+          listed = n < m0 ? all : (all & ~((1u << (n - m0)) - 1u));
+        } else if (n < sd0) {
+          listed = (cur.bits >> (7 - (cur.ti.w & 7))) & 1u ? all : 0u;
+        } else {
+          listed = cur.bits;
+          const int j = n - sd0;
+          if (j >= i && j < i + nb) listed |= 1u << (j - i);  // the diagonal tile
+        }
+      }
+      e.emit_at(listed, n, cur.row0, cur.ti.y);
+      cur = nxt;
     }
-  } else if (grouped && pt.seg_kind[s] == kQuery) {
+  } else if (pt.seg_kind[s] == kQuery) {
     // the same, segment by segment so that tile groups stay within one call
     for (int d = pt.seg_first[s]; d <= s; ++d) {
       const int last = d < s ? pt.seg_pages[d] - 1 : mlast - pt.seg_tile0[s];
@@ -326,17 +404,15 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
       }
     }
   } else {
-    // CA pages of every earlier document: the same for all M-blocks
+    // T < 64, a document unit.  CA pages of every earlier document: the
+    // same for all M-blocks
     for (int d = pt.seg_first[s]; d < s; ++d) {
       const int Pe = pt.seg_pages[d];
       const uint8_t* cav = ca + pt.seg_ca_off[d] + static_cast<int64_t>(h) * ca_nbytes(Pe);
       for (int c0 = 0; c0 < Pe; c0 += 64) {
         const int b = c0 + lane;
         const bool on = b < Pe && get_bit(cav, b);
-        if constexpr (grouped)
-          e.emit_grouped(on ? all : 0u, pt.seg_tile0[d] + b, b, Pe, lane);
-        else
-          e.emit(on ? all : 0u, pt.seg_tile0[d] + b);
+        e.emit_grouped(on ? all : 0u, pt.seg_tile0[d] + b, b, Pe, lane);
       }
     }
     // LA rows i .. i+nb-1 of the document's triangle, tiles j = 0 .. i+nb-1;
@@ -352,10 +428,7 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
         const int r = i + k;
         if (k < nb && j <= r && (j == r || get_bit(lav, r * (r + 1) / 2 + j))) listed |= 1u << k;
       }
-      if constexpr (grouped)
-        e.emit_grouped(listed, pt.seg_tile0[s] + j, j, P, lane);
-      else
-        e.emit(listed, pt.seg_tile0[s] + j);
+      e.emit_grouped(listed, pt.seg_tile0[s] + j, j, P, lane);
     }
   }
   const int32_t cnt = e.ps - e.base;
@@ -484,17 +557,21 @@ __global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
   write_work_counts(wt, wt.lu_work0[u], wt.lu_nwork[u], plen, ns, 0, 1);
 }
 
-// Schedule pass, block x for chunk x: scan the chunk's bucket sizes (one
-// bucket per thread) into offsets, clear them, then place every work unit of
-// the chunk at launch[x + kNumXcd * k], k taken from its bucket's offset
-// with an LDS atomic (equal counts land in any order).
+// Schedule pass, blocks x sched_blocks .. for chunk x: each scans the
+// chunk's bucket sizes (one bucket per thread) into offsets, then copies its
+// share of the chunk's work units to launch[x + kNumXcd * k], k = the offset
+// of the unit's bucket plus its rank in the bucket.  The chunk's last block
+// to finish clears its buckets for the next decode.
 __global__ __launch_bounds__(1024) void schedule_scatter(WorkTables wt) {
   __shared__ int32_t off[kSchedBuckets];
   __shared__ int32_t wsum[16];
+  __shared__ int last;
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int wave = t >> 6;
-  const int x = blockIdx.x;
+  const int nbk = wt.sched_blocks;
+  const int x = blockIdx.x / nbk;
+  const int part = blockIdx.x - x * nbk;
   int32_t* hist = wt.hist + x * kSchedBuckets;
   const int32_t own = hist[t];
   int32_t s = own;  // inclusive scan inside the wavefront
@@ -507,42 +584,38 @@ __global__ __launch_bounds__(1024) void schedule_scatter(WorkTables wt) {
   int32_t e = s - own;
   for (int j = 0; j < wave; ++j) e += wsum[j];
   off[t] = e;
-  hist[t] = 0;  // only this block reads the chunk's buckets
   __syncthreads();
-  // kBatch work units per thread at a time, their loads issued together
-  constexpr int kBatch = 4;
-  const int32_t w_end = min(wt.num_work, (x + 1) * wt.chunk_size);
-  for (int32_t w0 = x * wt.chunk_size; w0 < w_end; w0 += kBatch * 1024) {
-    int4 r[kBatch][4];
+  const int32_t c0 = x * wt.chunk_size;
+  const int32_t c1 = min(wt.num_work, c0 + wt.chunk_size);
+  const int32_t per = (wt.chunk_size + nbk - 1) / nbk;
+  const int32_t w_end = min(c1, c0 + (part + 1) * per);
+  for (int32_t w = c0 + part * per + t; w < w_end; w += 1024) {
+    const int4* src = reinterpret_cast<const int4*>(wt.rec + w);
+    int4 r[4];
 #pragma unroll
-    for (int b = 0; b < kBatch; ++b) {
-      const int32_t w = w0 + b * 1024 + t;
-      if (w < w_end) {
-        const int4* src = reinterpret_cast<const int4*>(wt.rec + w);
+    for (int q = 0; q < 4; ++q) r[q] = src[q];
+    // the step count is word 9 of the record (int4 2, .y), the rank word 2
+    const int32_t k = off[sched_bucket(r[2].y)] + r[0].z;
+    if (k >= 0 && k < wt.chunk_size) {
+      int4* dst = reinterpret_cast<int4*>(wt.launch + x + kNumXcd * k);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) r[b][q] = src[q];
-      }
+      for (int q = 0; q < 4; ++q) dst[q] = r[q];
     }
-#pragma unroll
-    for (int b = 0; b < kBatch; ++b) {
-      const int32_t w = w0 + b * 1024 + t;
-      if (w < w_end) {
-        // the step count is word 9 of the record (rc.y)
-        const int32_t k = atomicAdd(&off[sched_bucket(r[b][2].y)], 1);
-        if (k >= 0 && k < wt.chunk_size) {
-          int4* dst = reinterpret_cast<int4*>(wt.launch + x + kNumXcd * k);
-#pragma unroll
-          for (int q = 0; q < 4; ++q) dst[q] = r[b][q];
-        }
-      }
-    }
+  }
+  // every block of the chunk has read the buckets once the last one is here
+  if (t == 0) last = atomicAdd(&wt.sched_done[x], 1) == nbk - 1;
+  __syncthreads();
+  if (last) {
+    hist[t] = 0;
+    if (t == 0) wt.sched_done[x] = 0;
   }
 }
 
 hipError_t launch_schedule(const WorkTables& wt, hipStream_t stream) {
   if (wt.num_work == 0) return hipSuccess;
   static_assert(kSchedBuckets == 1024, "one bucket per thread of the schedule pass");
-  hipLaunchKernelGGL(schedule_scatter, dim3(kNumXcd), dim3(1024), 0, stream, wt);
+  hipLaunchKernelGGL(schedule_scatter, dim3(kNumXcd * wt.sched_blocks), dim3(1024), 0, stream,
+                     wt);
   return hipGetLastError();
 }
 

@@ -83,6 +83,7 @@ sift_status check_io(const sift_tensor* q, const sift_tensor* k, const sift_tens
 struct HostPlan {
   std::vector<int32_t> seg_tile0, seg_pages, seg_kind, seg_first, seg_la_off, seg_ca_off;
   std::vector<int32_t> tile_seg, tile_tok0, tile_len, tile_lo;
+  std::vector<int32_t> tile_info;  // int4 per tile (see PlanTables::tile_info)
   std::vector<int32_t> unit_head, unit_m0, unit_nb, step_off;  // list units
   std::vector<int32_t> lu_work0, lu_nwork, lu_len;
   std::vector<int32_t> wk_head, wk_m0, wk_nb, wk_off, wk_slot;        // work units
@@ -155,15 +156,23 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
   hp.tile_tok0.resize(tiles);
   hp.tile_len.resize(tiles);
   hp.tile_lo.resize(tiles);
+  hp.tile_info.resize(4 * tiles);
   for (int32_t b = 0; b < B; ++b) {
     const int32_t lo = hp.seg_tile0[psp[b]];
     for (int32_t s = psp[b]; s < psp[b + 1]; ++s) {
-      for (int32_t i = 0; i < hp.seg_pages[s]; ++i) {
+      const bool doc = hp.seg_kind[s] == sift::kDocument;
+      const int32_t P = hp.seg_pages[s];
+      for (int32_t i = 0; i < P; ++i) {
         const int32_t m = hp.seg_tile0[s] + i;
         hp.tile_seg[m] = s;
         hp.tile_tok0[m] = so[s] + i * tile;
         hp.tile_len[m] = std::min<int32_t>(tile, so[s + 1] - (so[s] + i * tile));
         hp.tile_lo[m] = lo;
+        int32_t* ti = &hp.tile_info[4 * static_cast<int64_t>(m)];
+        ti[0] = hp.tile_tok0[m];
+        ti[1] = hp.tile_len[m];
+        ti[2] = doc ? hp.seg_ca_off[s] + (i >> 3) : -1;
+        ti[3] = doc ? static_cast<int32_t>(ca_nbytes(P) << 3) | (i & 7) : 0;
       }
     }
   }
@@ -284,8 +293,8 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
     if (halves == 1) {
       // kernel block b: M-blocks m0 + G b .. m0 + G b + G - 1 of the unit
       const int32_t m0 = hp.wk_m0[w], nb = hp.wk_nb[w];
-      r.nb = (nb + G - 1) / G;
-      for (int b = 0; b < r.nb; ++b) {
+      const int32_t blocks = (nb + G - 1) / G;
+      for (int b = 0; b < blocks; ++b) {
         r.tok0[b] = hp.tile_tok0[m0 + G * b];
         r.len[b] = 0;
         for (int32_t m = m0 + G * b; m < std::min(m0 + nb, m0 + G * b + G); ++m)
@@ -293,7 +302,6 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
       }
     } else {  // one M-block of T = 128: two kernel blocks of 64 rows
       const int32_t m = hp.wk_m0[w], len = hp.tile_len[m];
-      r.nb = len > 64 ? 2 : 1;
       r.tok0[0] = hp.tile_tok0[m];
       r.len[0] = std::min<int32_t>(len, 64);
       r.tok0[1] = len > 64 ? hp.tile_tok0[m] + 64 : 0;
@@ -305,7 +313,6 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
   // schedule pass fills those of the work units
   hp.chunk_size = (W + sift::kNumXcd - 1) / sift::kNumXcd;
   sift::WorkRec empty{};
-  empty.nb = 1;
   empty.slot = -1;
   hp.launch.assign(hp.chunk_size * sift::kNumXcd, empty);
   return SIFT_OK;
@@ -433,6 +440,7 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   const size_t o_tile_tok0 = put(blob, hp.tile_tok0);
   const size_t o_tile_len = put(blob, hp.tile_len);
   const size_t o_tile_lo = put(blob, hp.tile_lo);
+  const size_t o_tile_info = put(blob, hp.tile_info);
   const size_t o_uh = put(blob, hp.unit_head);
   const size_t o_um0 = put(blob, hp.unit_m0);
   const size_t o_unb = put(blob, hp.unit_nb);
@@ -446,7 +454,7 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   // the schedule's bucket sizes, the bf16 attention's redo flag and
   // counters, the decode's finished-block count: zeros, uploaded with the
   // tables
-  constexpr size_t kHistWords = sift::kNumXcd * sift::kSchedBuckets + 4;
+  constexpr size_t kHistWords = sift::kNumXcd * sift::kSchedBuckets + 4 + sift::kNumXcd;
   const size_t o_hist = put(blob, std::vector<int32_t>(kHistWords, 0));
   const int64_t rows = static_cast<int64_t>(hp.num_tiles) * num_q_heads;
   const int64_t cap = hp.dense_tiles * num_q_heads;
@@ -530,6 +538,7 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   plan->pt.tile_tok0 = P(o_tile_tok0);
   plan->pt.tile_len = P(o_tile_len);
   plan->pt.tile_lo = P(o_tile_lo);
+  plan->pt.tile_info = reinterpret_cast<const int4*>(P(o_tile_info));
   plan->pt.tile = tile;
   plan->pt.halves = tile == 128 ? 2 : 1;
   plan->pt.group = tile < 64 ? 64 / tile : 1;
@@ -554,11 +563,14 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   plan->wt.part_ml = reinterpret_cast<float2*>(P(o_part_ml));
   plan->wt.redo = P(o_hist) + sift::kNumXcd * sift::kSchedBuckets;
   plan->wt.decode_done = plan->wt.redo + 3;
+  plan->wt.sched_done = plan->wt.redo + 4;
   plan->wt.seg_base = P(o_segbase);
   plan->wt.num_units = static_cast<int32_t>(U);
   plan->wt.num_work = static_cast<int32_t>(W);
   plan->wt.num_splits = static_cast<int32_t>(hp.splits.size() / 4);
   plan->wt.chunk_size = static_cast<int32_t>(hp.chunk_size);
+  plan->wt.sched_blocks = static_cast<int32_t>(
+      std::min<int64_t>(8, std::max<int64_t>(1, ceil_div(hp.chunk_size, sift::kSchedPerBlock))));
   plan->wt.grid = static_cast<int32_t>(hp.launch.size());
   plan->counts = P(o_counts);
   plan->row_ptr = P(o_rowptr);

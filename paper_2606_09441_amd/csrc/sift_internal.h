@@ -24,6 +24,9 @@ struct PlanTables {
   const int32_t* tile_tok0;   // first token of tile m on the packed axis
   const int32_t* tile_len;    // tokens in tile m (T, or less for a last tile)
   const int32_t* tile_lo;     // first tile of m's prompt
+  const int4* tile_info;      // {tok0, len, byte offset of query head 0's CA byte holding the
+                              // tile's bit (-1: a query tile), CA bytes per head << 3 | bit
+                              // position in the byte}: what decode reads per candidate tile
   int32_t num_tiles;          // M
   int32_t num_segments;       // S
   int32_t num_q_heads;        // Hq
@@ -80,15 +83,18 @@ __device__ __forceinline__ int32_t kv_row0(const PlanTables& pt, const KvPages& 
 // that copies each record to launch[x + kNumXcd * k], k its place in that
 // order (launch slots past a chunk's end hold an empty record: one M-block
 // of no rows, no steps).  The order is a counting sort: decode counts the
-// work units of each (chunk, step count) bucket in hist[]; the schedule
-// pass, one block per chunk, scans the chunk's buckets, places each work
-// unit with an LDS atomic on its bucket's offset, and clears the buckets.
+// work units of each (chunk, step count) bucket in hist[], keeping each
+// unit's place in its bucket (rank); the schedule pass, sched_blocks blocks
+// per chunk, scans the chunk's buckets and copies every work unit to its
+// bucket's offset plus its rank; the chunk's last block clears the buckets.
 constexpr int kNumXcd = 8;  // MI355X
 constexpr int kUnitBlocks = 2;                 // 64-row kernel blocks of a unit
 constexpr int kUnitRows = 64 * kUnitBlocks;  // query rows of a unit
 constexpr int kMaxListBlocks = 8;            // M-blocks of a list unit: 128 / T, at most 8 (T = 16)
 constexpr int kFirstSteps = 3;
 constexpr int kSchedBuckets = 1024;          // step counts >= 1023 share bucket 0
+constexpr int kSchedPerBlock = 1024;         // work units per schedule block (at most 8
+                                             // blocks per chunk)
 
 // Bucket of a step count: decreasing counts in increasing bucket order.
 __device__ __forceinline__ int32_t sched_bucket(int32_t cnt) {
@@ -98,7 +104,8 @@ __device__ __forceinline__ int32_t sched_bucket(int32_t cnt) {
 struct alignas(64) WorkRec {
   int32_t head;      // query head
   int32_t kv_head;   // its K/V head
-  int32_t nb;        // M-blocks, 1 .. kUnitBlocks
+  int32_t rank;      // place among the work units of its (chunk, step-count bucket), in
+                     // the order decode counted them (written by decode)
   int32_t slot;      // partial slot, or -1: write the output
   int32_t tok0[kUnitBlocks];  // first token of each M-block (0 when absent)
   int32_t len[kUnitBlocks];   // tokens of each M-block (0 when absent)
@@ -109,6 +116,7 @@ struct alignas(64) WorkRec {
 };
 static_assert(sizeof(WorkRec) == 64, "one record per 64 bytes");
 static_assert(offsetof(WorkRec, step_cnt) == 36, "the step count is word 9 (read as int4 2, .y)");
+static_assert(offsetof(WorkRec, rank) == 8, "the rank is word 2 (read as int4 0, .z)");
 
 struct WorkTables {
   WorkRec* rec;               // [W] locality order (device memory)
@@ -134,6 +142,8 @@ struct WorkTables {
                               // then their first list entry (device scratch)
   int32_t* decode_done;       // decode: finished count blocks (device scratch, zero between
                               // decodes)
+  int32_t* sched_done;        // [kNumXcd] schedule: finished blocks per chunk (device
+                              // scratch, zero between decodes)
   int32_t* redo;              // [3] bf16 attention: {flag: do every unit again exactly,
                               // finished workgroups of that pass (both zero between
                               // launches), launches whose exact pass ran (a count kept
@@ -142,6 +152,7 @@ struct WorkTables {
   int32_t num_work;           // W
   int32_t num_splits;         // NS
   int32_t chunk_size;         // work units per XCD chunk
+  int32_t sched_blocks;       // schedule blocks per chunk
   int32_t grid;               // kNumXcd * chunk_size
 };
 
@@ -155,7 +166,7 @@ __device__ __forceinline__ void write_work_counts(const WorkTables& wt, int32_t 
     const int32_t c = rest < 0 ? 0 : (rest > len ? len : rest);
     wt.rec[w0 + k].step_cnt = c;
     const int32_t x = (w0 + k) / wt.chunk_size;
-    atomicAdd(&wt.hist[x * kSchedBuckets + sched_bucket(c)], 1);
+    wt.rec[w0 + k].rank = atomicAdd(&wt.hist[x * kSchedBuckets + sched_bucket(c)], 1);
   }
 }
 
@@ -176,13 +187,12 @@ struct TileSteps {
   int2 s[2];
 };
 
-__device__ __forceinline__ TileSteps tile_steps(const PlanTables& pt, const KvPages& pg, int32_t n,
-                                                unsigned listed, int32_t m0, int32_t nb) {
+__device__ __forceinline__ TileSteps tile_steps_at(const PlanTables& pt, int32_t n, unsigned listed,
+                                                   int32_t m0, int32_t nb, int32_t row0,
+                                                   int32_t len) {
   TileSteps t;
   t.cnt = 0;
   if (listed == 0u) return t;
-  const int32_t row0 = kv_row0(pt, pg, n);
-  const int32_t len = pt.tile_len[n];
   if (pt.halves == 1) {
     const unsigned diag = (n >= m0 && n < m0 + nb) ? 1u << (n - m0) : 0u;
     t.cnt = 1;
@@ -201,6 +211,12 @@ __device__ __forceinline__ TileSteps tile_steps(const PlanTables& pt, const KvPa
                                       static_cast<int>((d0 << 1) << kStepDiagShift));
   }
   return t;
+}
+
+__device__ __forceinline__ TileSteps tile_steps(const PlanTables& pt, const KvPages& pg, int32_t n,
+                                                unsigned listed, int32_t m0, int32_t nb) {
+  if (listed == 0u) return TileSteps{0, {}};
+  return tile_steps_at(pt, n, listed, m0, nb, kv_row0(pt, pg, n), pt.tile_len[n]);
 }
 
 // Decode (Section 5.1): count, write, schedule.  The count pass writes each
