@@ -83,6 +83,96 @@ __device__ __forceinline__ int32_t block_scan256(int32_t v, int32_t& incl, int32
   return total;
 }
 
+// Inclusive scan of v over the 1024 threads of a block (wavefront scans,
+// then the 16 wavefront totals through LDS); returns the block total.
+__device__ __forceinline__ int32_t block_scan1024(int32_t v, int32_t& incl, int32_t* wtot) {
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  int32_t x = v;
+  for (int off = 1; off < 64; off <<= 1) {
+    const int32_t y = __shfl_up(x, off, 64);
+    if (lane >= off) x += y;
+  }
+  if (lane == 63) wtot[w] = x;
+  __syncthreads();
+  int32_t before = 0, total = 0;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    before += j < w ? wtot[j] : 0;
+    total += wtot[j];
+  }
+  __syncthreads();
+  incl = before + x;
+  return total;
+}
+
+constexpr int kCountSegs = 1024;  // segments the per-head count pass holds in LDS
+
+// Block h: every row of query head h (layouts of at most kCountSegs
+// segments).  A document row i lists the marked pages of the earlier
+// documents of its prompt, the marked tiles j < i of its LA row and its
+// diagonal; a query row lists every tile of its prompt up to its own
+// (Section 5.1).  First each document's CA popcount for head h, then, per
+// prompt, what each of its segments' rows see of the earlier documents
+// (in LDS); then the rows, scanned in tile order: local[] gets each row's
+// offset inside head h, head_tot[h] the head's total.  The write pass adds
+// the totals of the heads before h.
+__global__ __launch_bounds__(1024) void decode_count_head(PlanTables pt, WorkTables wt,
+                                                          const uint8_t* __restrict__ la,
+                                                          const uint8_t* __restrict__ ca,
+                                                          int32_t* __restrict__ local) {
+  __shared__ int32_t cross[kCountSegs];  // CA popcount, then the pages a row of s sees
+  __shared__ int32_t first[kCountSegs];  // first segment of the prompt
+  __shared__ int32_t wtot[16];
+  const int S = pt.num_segments;
+  const int M = pt.num_tiles;
+  const int h = blockIdx.x;
+  const int t = threadIdx.x;
+  // the first rows' segments, issued early (independent of what follows)
+  int seg0 = t < M ? pt.tile_seg[t] : 0;
+  for (int s = t; s < S; s += 1024) {
+    const int P = pt.seg_pages[s];
+    first[s] = pt.seg_first[s];
+    cross[s] = pt.seg_kind[s] == kQuery
+                   ? 0
+                   : popc_bits(ca + pt.seg_ca_off[s] + static_cast<int64_t>(h) * ca_nbytes(P), 0, P);
+  }
+  __syncthreads();
+  // per prompt, in segment order: each segment's rows see the pages its
+  // earlier documents mark (a query's rows are counted in closed form)
+  for (int s = t; s < S; s += 1024) {
+    if (first[s] != s) continue;  // one thread per prompt
+    int32_t run = 0;
+    for (int e = s; e < S && first[e] == s; ++e) {
+      const int32_t v = cross[e];
+      cross[e] = run;
+      run += v;
+    }
+  }
+  __syncthreads();
+  int32_t* lrow = local + static_cast<int64_t>(h) * M;
+  int32_t run = 0;
+  for (int m0 = 0; m0 < M; m0 += 1024) {
+    const int m = m0 + t;
+    int32_t cnt = 0;
+    if (m < M) {
+      const int s = m0 == 0 ? seg0 : pt.tile_seg[m];
+      const int i = m - pt.seg_tile0[s];
+      if (pt.seg_kind[s] == kQuery) {
+        cnt = m - pt.seg_tile0[first[s]] + 1;
+      } else {
+        const int P = pt.seg_pages[s];
+        const uint8_t* lav = la + pt.seg_la_off[s] + static_cast<int64_t>(h) * la_nbytes(P);
+        cnt = cross[s] + 1 + popc_bits(lav, i * (i + 1) / 2, i);
+      }
+    }
+    int32_t incl;
+    const int32_t chunk = block_scan1024(cnt, incl, wtot);
+    if (m < M) lrow[m] = run + incl - cnt;
+    run += chunk;
+  }
+  if (t == 0) wt.head_tot[h] = run;
+}
+
 // Block b = h S + s: the rows of segment s for query head h.  A document row
 // i lists the marked pages of the earlier documents of its prompt, the
 // marked tiles j < i of its LA row and its diagonal; a query row lists every
@@ -317,7 +407,25 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   e.pt = &pt;
   e.pages = pages;
   const int s = pt.tile_seg[m0];
-  const int32_t base = wt.seg_base[h * pt.num_segments + s];
+  int32_t base;
+  if (wt.head_tot != nullptr) {
+    // local[] holds offsets inside the head: add the totals of heads 0 .. h-1
+    int32_t before = 0, nnz = 0;
+    for (int j0 = 0; j0 < pt.num_q_heads; j0 += 64) {
+      const int j = j0 + lane;
+      const int32_t v = j < pt.num_q_heads ? wt.head_tot[j] : 0;
+      before += j < h ? v : 0;
+      nnz += v;
+    }
+    for (int off = 32; off > 0; off >>= 1) {
+      before += __shfl_xor(before, off, 64);
+      nnz += __shfl_xor(nnz, off, 64);
+    }
+    base = before;
+    if (u == 0 && lane == 0) row_ptr[static_cast<int64_t>(pt.num_q_heads) * pt.num_tiles] = nnz;
+  } else {
+    base = wt.seg_base[h * pt.num_segments + s];
+  }
 #pragma unroll
   for (int k = 0; k < kNb; ++k) {
     e.pos[k] = k < nb ? base + local[r0 + k] : 0;
@@ -624,29 +732,40 @@ hipError_t launch_schedule(const WorkTables& wt, hipStream_t stream) {
 hipError_t launch_decode(const PlanTables& pt, const WorkTables& wt, const uint8_t* la,
                          const uint8_t* ca, int32_t* counts, int32_t* row_ptr, int32_t* col_idx,
                          const KvPages& pages, hipStream_t stream) {
-  // one count block per (head, segment); the last one also writes row_ptr[Hq M]
-  const int64_t blocks = static_cast<int64_t>(pt.num_q_heads) * pt.num_segments;
-  hipLaunchKernelGGL(decode_count, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, pt,
-                     wt, la, ca, counts, row_ptr);
-  hipError_t e = hipGetLastError();
+  hipError_t e;
+  WorkTables w2 = wt;
+  if (pt.num_segments <= kCountSegs && wt.num_units > 0) {
+    // one count block per head; the write pass adds the heads' totals and
+    // writes row_ptr[Hq M]
+    hipLaunchKernelGGL(decode_count_head, dim3(static_cast<unsigned>(pt.num_q_heads)), dim3(1024),
+                       0, stream, pt, wt, la, ca, counts);
+  } else {
+    // one count block per (head, segment); the last one scans the totals
+    // and writes row_ptr[Hq M]
+    w2.head_tot = nullptr;
+    const int64_t blocks = static_cast<int64_t>(pt.num_q_heads) * pt.num_segments;
+    hipLaunchKernelGGL(decode_count, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, pt,
+                       wt, la, ca, counts, row_ptr);
+  }
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (wt.num_units == 0) return hipSuccess;
   const dim3 wgrid(static_cast<unsigned>((wt.num_units + 3) / 4));
   if (pt.group == 4)
-    hipLaunchKernelGGL((decode_write<8, true, false>), wgrid, dim3(256), 0, stream, pt, wt, la, ca,
+    hipLaunchKernelGGL((decode_write<8, true, false>), wgrid, dim3(256), 0, stream, pt, w2, la, ca,
                        counts, row_ptr, col_idx, pages);
   else if (pt.group == 2)
-    hipLaunchKernelGGL((decode_write<4, true, false>), wgrid, dim3(256), 0, stream, pt, wt, la, ca,
+    hipLaunchKernelGGL((decode_write<4, true, false>), wgrid, dim3(256), 0, stream, pt, w2, la, ca,
                        counts, row_ptr, col_idx, pages);
   else if (pt.halves == 2)
-    hipLaunchKernelGGL((decode_write<2, false, true>), wgrid, dim3(256), 0, stream, pt, wt, la, ca,
+    hipLaunchKernelGGL((decode_write<2, false, true>), wgrid, dim3(256), 0, stream, pt, w2, la, ca,
                        counts, row_ptr, col_idx, pages);
   else
-    hipLaunchKernelGGL((decode_write<2, false, false>), wgrid, dim3(256), 0, stream, pt, wt, la, ca,
+    hipLaunchKernelGGL((decode_write<2, false, false>), wgrid, dim3(256), 0, stream, pt, w2, la, ca,
                        counts, row_ptr, col_idx, pages);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return launch_schedule(wt, stream);
+  return launch_schedule(w2, stream);
 }
 
 hipError_t launch_merge_steps(const PlanTables& pt, const WorkTables& wt, const int32_t* row_ptr,

@@ -462,7 +462,8 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
   const size_t o_counts = align(blob.size());
   const size_t o_segbase = align(o_counts + rows * 4);
-  const size_t o_rowptr = align(o_segbase + static_cast<int64_t>(hp.num_segments) * num_q_heads * 4);
+  const size_t o_headtot = align(o_segbase + static_cast<int64_t>(hp.num_segments) * num_q_heads * 4);
+  const size_t o_rowptr = align(o_headtot + static_cast<int64_t>(num_q_heads) * 4);
   const size_t o_col = align(o_rowptr + (rows + 1) * 4);
   const int64_t W = static_cast<int64_t>(hp.wk_head.size());
   const size_t o_steps = align(o_col + std::max<int64_t>(cap, 1) * 4);
@@ -565,6 +566,7 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   plan->wt.decode_done = plan->wt.redo + 3;
   plan->wt.sched_done = plan->wt.redo + 4;
   plan->wt.seg_base = P(o_segbase);
+  plan->wt.head_tot = P(o_headtot);
   plan->wt.num_units = static_cast<int32_t>(U);
   plan->wt.num_work = static_cast<int32_t>(W);
   plan->wt.num_splits = static_cast<int32_t>(hp.splits.size() / 4);

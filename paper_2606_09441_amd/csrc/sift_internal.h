@@ -142,6 +142,7 @@ struct WorkTables {
                               // then their first list entry (device scratch)
   int32_t* decode_done;       // decode: finished count blocks (device scratch, zero between
                               // decodes)
+  int32_t* head_tot;          // [Hq] decode: each query head's list entries (device scratch)
   int32_t* sched_done;        // [kNumXcd] schedule: finished blocks per chunk (device
                               // scratch, zero between decodes)
   int32_t* redo;              // [3] bf16 attention: {flag: do every unit again exactly,
