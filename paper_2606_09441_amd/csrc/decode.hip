@@ -113,13 +113,18 @@ constexpr int kCountSegs = 1024;  // segments the per-head count pass holds in L
 // diagonal; a query row lists every tile of its prompt up to its own
 // (Section 5.1).  First each document's CA popcount for head h, then, per
 // prompt, what each of its segments' rows see of the earlier documents
-// (in LDS); then the rows, scanned in tile order: local[] gets each row's
-// offset inside head h, head_tot[h] the head's total.  The write pass adds
-// the totals of the heads before h.
+// (in LDS, and to seg_cross); then the rows, scanned in tile order: local[]
+// gets each row's offset inside head h, head_tot[h] the head's total.  The
+// write pass adds the totals of the heads before h.
+// The CA-marked tiles of a prompt, in tile order, also go to the head's
+// cross list (from the prompt's first tile on: there are fewer marked tiles
+// than tiles): the earlier documents' part of a document row's list is a
+// prefix of it, which the write pass copies instead of walking every page.
 __global__ __launch_bounds__(1024) void decode_count_head(PlanTables pt, WorkTables wt,
                                                           const uint8_t* __restrict__ la,
                                                           const uint8_t* __restrict__ ca,
-                                                          int32_t* __restrict__ local) {
+                                                          int32_t* __restrict__ local,
+                                                          KvPages pages) {
   __shared__ int32_t cross[kCountSegs];  // CA popcount, then the pages a row of s sees
   __shared__ int32_t first[kCountSegs];  // first segment of the prompt
   __shared__ int32_t wtot[16];
@@ -145,6 +150,7 @@ __global__ __launch_bounds__(1024) void decode_count_head(PlanTables pt, WorkTab
     for (int e = s; e < S && first[e] == s; ++e) {
       const int32_t v = cross[e];
       cross[e] = run;
+      wt.seg_cross[h * S + e] = run;
       run += v;
     }
   }
@@ -157,13 +163,23 @@ __global__ __launch_bounds__(1024) void decode_count_head(PlanTables pt, WorkTab
     if (m < M) {
       const int s = m0 == 0 ? seg0 : pt.tile_seg[m];
       const int i = m - pt.seg_tile0[s];
+      uint8_t mk = 0;
       if (pt.seg_kind[s] == kQuery) {
         cnt = m - pt.seg_tile0[first[s]] + 1;
       } else {
         const int P = pt.seg_pages[s];
         const uint8_t* lav = la + pt.seg_la_off[s] + static_cast<int64_t>(h) * la_nbytes(P);
+        const uint8_t* cav = ca + pt.seg_ca_off[s] + static_cast<int64_t>(h) * ca_nbytes(P);
+        mk = static_cast<uint8_t>(get_bit(cav, i));
+        const int32_t before = popc_bits(cav, 0, i);  // marked pages of s before i
         cnt = cross[s] + 1 + popc_bits(lav, i * (i + 1) / 2, i);
+        if (mk != 0) {
+          const int64_t y = static_cast<int64_t>(h) * M + pt.seg_tile0[first[s]] + cross[s] + before;
+          wt.cross_col[y] = m;
+          wt.cross_rows[y] = make_int2(kv_row0(pt, pages, m), pt.tile_len[m]);
+        }
       }
+      wt.ca_mark[static_cast<int64_t>(h) * M + m] = mk;
     }
     int32_t incl;
     const int32_t chunk = block_scan1024(cnt, incl, wtot);
@@ -195,16 +211,22 @@ __global__ __launch_bounds__(256) void decode_count(PlanTables pt, WorkTables wt
   const int P = pt.seg_pages[s];
   const int tile0 = pt.seg_tile0[s];
   int32_t* lrow = local + static_cast<int64_t>(h) * pt.num_tiles + tile0;
+  uint8_t* mrow = wt.ca_mark + static_cast<int64_t>(h) * pt.num_tiles + tile0;
   int32_t total;
   if (pt.seg_kind[s] == kQuery) {
     // row i lists a + i tiles, a = the tiles before the segment plus one
     const int a = tile0 - pt.seg_tile0[pt.seg_first[s]] + 1;
-    for (int i = t; i < P; i += 256) lrow[i] = i * a + i * (i - 1) / 2;
+    for (int i = t; i < P; i += 256) {
+      lrow[i] = i * a + i * (i - 1) / 2;
+      mrow[i] = 0;
+    }
     total = P * a + P * (P - 1) / 2;
   } else {
     // marked pages of the earlier documents (the same for every row) and
     // the LA bits of each row before its diagonal: all loads issued first
     const uint8_t* lav = la + pt.seg_la_off[s] + static_cast<int64_t>(h) * la_nbytes(P);
+    const uint8_t* cav = ca + pt.seg_ca_off[s] + static_cast<int64_t>(h) * ca_nbytes(P);
+    for (int i = t; i < P; i += 256) mrow[i] = static_cast<uint8_t>(get_bit(cav, i));
     int32_t c = 0;
     for (int e = pt.seg_first[s] + t; e < s; e += 256) {
       const int Pe = pt.seg_pages[e];
@@ -292,6 +314,7 @@ struct Emitter {
   int32_t pos[kNb];  // next write position in each M-block's list
   int32_t ps;                   // next write position in the step list
   int32_t m0, nb;
+  unsigned hrows;  // T = 128: kernel blocks of the M-block (tile_steps_at)
   unsigned long long below;
 
   __device__ __forceinline__ void lists(unsigned listed, int32_t n) {
@@ -324,7 +347,7 @@ struct Emitter {
       return;
     }
     // one or two steps per listed tile, in lane order
-    const TileSteps ts = tile_steps_at(*pt, n, listed, m0, nb, row0, len);
+    const TileSteps ts = tile_steps_at(*pt, n, listed, m0, nb, row0, len, hrows);
     const unsigned long long mu1 = __ballot(ts.cnt >= 1), mu2 = __ballot(ts.cnt >= 2);
     const int32_t idx = ps + __popcll(mu1 & below) + __popcll(mu2 & below);
     for (int q = 0; q < ts.cnt; ++q) {
@@ -332,6 +355,45 @@ struct Emitter {
       if (whole && idx + q - base < kFirstSteps) wt->rec[w0].first[idx + q - base] = ts.s[q];
     }
     ps += __popcll(mu1) + __popcll(mu2);
+  }
+
+  // One round of a document unit's earlier-document part, copied from the
+  // head's cross list: the first cnt lanes hold a CA-marked tile (id c,
+  // {first row, length} r), listed by every M-block; at T = 64 one step
+  // each, at T = 128 one per 64 keys.
+  __device__ __forceinline__ void copy_round(int32_t c, int2 r, int32_t cnt, int lane) {
+    const bool valid = lane < cnt;
+    const unsigned lst = kHalves ? hrows : (1u << nb) - 1u;
+    const int info_or = static_cast<int>(lst << kStepListedShift);
+#pragma unroll
+    for (int k = 0; k < kNb; ++k) {
+      if (k >= nb) break;
+      if (valid) col[pos[k] + lane] = c;
+      pos[k] += cnt;
+    }
+    if constexpr (!kHalves) {
+      if (valid) {
+        const int2 st = make_int2(r.x, r.y | info_or);
+        steps[ps + lane] = st;
+        if (whole && ps + lane - base < kFirstSteps) wt->rec[w0].first[ps + lane - base] = st;
+      }
+      ps += cnt;
+    } else {
+      const bool two = valid && r.y > 64;
+      const unsigned long long m2 = __ballot(two);
+      const int32_t idx = ps + lane + __popcll(m2 & below);
+      if (valid) {
+        const int2 s0 = make_int2(r.x, min(r.y, 64) | info_or);
+        steps[idx] = s0;
+        if (whole && idx - base < kFirstSteps) wt->rec[w0].first[idx - base] = s0;
+        if (two) {
+          const int2 s1 = make_int2(r.x + 64, (r.y - 64) | info_or);
+          steps[idx + 1] = s1;
+          if (whole && idx + 1 - base < kFirstSteps) wt->rec[w0].first[idx + 1 - base] = s1;
+        }
+      }
+      ps += cnt + __popcll(m2);
+    }
   }
 
   // T < 64.  The lanes hold tiles local = c0 + lane of one segment of P
@@ -394,19 +456,93 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
                                                     int32_t* __restrict__ row_ptr,
                                                     int32_t* __restrict__ col, KvPages pages) {
   const int lane = threadIdx.x & 63;
-  const int u = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (u >= wt.num_units) return;  // uniform per wavefront
-  const int h = wt.lu_head[u];
-  const int m0 = wt.lu_m0[u];
-  const int nb = wt.lu_nb[u];
+  const int slot = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
+  if (slot >= wt.num_units) return;  // uniform per wavefront
+  const UnitRec ur = wt.urec[slot];
+  const int h = ur.head, m0 = ur.m0, nb = ur.nb, s = ur.seg;
+  const int M = pt.num_tiles;
   const unsigned all = (1u << nb) - 1u;
-  const int64_t r0 = static_cast<int64_t>(h) * pt.num_tiles + m0;
+  const int64_t r0 = static_cast<int64_t>(h) * M + m0;
+  const int mlast = m0 + nb - 1;
+  // Every load that depends on the record alone is issued before any result
+  // is used: the rows' offsets, the first rounds of the candidate walk and
+  // of the cross-list copy, then the heads' totals.
+  int32_t loc[kNb];
+#pragma unroll
+  for (int k = 0; k < kNb; ++k) loc[k] = k < nb ? local[r0 + k] : 0;
+  //   T >= 64: the candidates are the prompt's tiles lo .. mlast in order
+  //   (the earlier documents' pages, then this segment's tiles), 64 per
+  //   round.  Query unit: M-block m0 + k lists n when n <= m0 + k (Section
+  //   5.1).  Document unit: every M-block lists the CA-marked pages of the
+  //   earlier documents (copied from the head's cross list when the count
+  //   pass built it), and row r = i + k its LA-marked tiles j < r and j == r.
+  //   Rounds go in chunks: a chunk's loads are all issued before any of
+  //   their results is used (raw bytes kept, bits taken later), so a chunk
+  //   waits on memory once.
+  constexpr int kChunk = 4, kCopy = 4;
+  const bool query = ur.query != 0;
+  const int lo = ur.lo, sd0 = ur.sd0, i = m0 - sd0;
+  const uint8_t* lav = query ? la : la + ur.la_off + static_cast<int64_t>(h) * la_nbytes(ur.pages);
+  const uint8_t* mark = wt.ca_mark + static_cast<int64_t>(h) * M;
+  const int2* rowlen = reinterpret_cast<const int2*>(pt.tile_info);  // {first row, length} at 2 n
+  const bool copy = !kGrouped && !query && wt.cross_col != nullptr;
+  const int64_t ybase = static_cast<int64_t>(h) * M + lo;
+  const int start = copy ? sd0 : lo;
+  int32_t ncross = 0;
+  int32_t yc[kCopy];
+  int2 yr[kCopy];
+  int2 tl[kChunk];
+  unsigned raw[kChunk][2];  // CA mark, or the LA bytes of rows i and i + 1
+  auto load_copy = [&](int t0) {
+#pragma unroll
+    for (int q = 0; q < kCopy; ++q) {
+      const int t = min(t0 + 64 * q + lane, M - 1 - lo);  // inside the head's list
+      yc[q] = wt.cross_col[ybase + t];
+      yr[q] = wt.cross_rows[ybase + t];
+    }
+  };
+  auto load_walk = [&](int c0) {
+    const int nr = min(kChunk, (mlast - c0) / 64 + 1);
+#pragma unroll
+    for (int c = 0; c < kChunk; ++c) {
+      if (c >= nr) break;
+      const int n = min(c0 + 64 * c + lane, mlast);
+      tl[c] = rowlen[2 * n];
+      if (pages.table != nullptr) tl[c].x = pages.table[n];
+      raw[c][0] = raw[c][1] = 0u;
+      if (!query) {
+        // every address valid: lav is the document's own LA vector
+        const int j = n - sd0;
+        const int b0 = i * (i + 1) / 2 + j, b1 = (i + 1) * (i + 2) / 2 + j;
+        const uint8_t* a0 = n < sd0 ? mark + n : (j < i ? lav + (b0 >> 3) : lav);
+        const uint8_t* a1 = (n >= sd0 && nb > 1 && j < i + 1) ? lav + (b1 >> 3) : lav;
+        raw[c][0] = *a0;
+        raw[c][1] = *a1;
+      }
+    }
+  };
+  if constexpr (!kGrouped) {
+    if (copy) {
+      ncross = wt.seg_cross[h * pt.num_segments + s];
+      load_copy(0);
+    }
+    load_walk(start);
+  }
   Emitter<kNb, kHalves> e;
   e.col = col;
   e.steps = wt.steps;
   e.pt = &pt;
+  e.wt = &wt;
   e.pages = pages;
-  const int s = pt.tile_seg[m0];
+  e.ps = ur.step_off;
+  e.base = e.ps;
+  const int32_t nw = ur.nwork, plen = ur.plen;  // pieces
+  e.w0 = ur.work0;
+  e.whole = nw == 1;
+  e.m0 = m0;
+  e.nb = nb;
+  e.hrows = static_cast<unsigned>(ur.hrows);
+  e.below = (1ull << lane) - 1ull;
   int32_t base;
   if (wt.head_tot != nullptr) {
     // local[] holds offsets inside the head: add the totals of heads 0 .. h-1
@@ -422,82 +558,55 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
       nnz += __shfl_xor(nnz, off, 64);
     }
     base = before;
-    if (u == 0 && lane == 0) row_ptr[static_cast<int64_t>(pt.num_q_heads) * pt.num_tiles] = nnz;
+    if (slot == 0 && lane == 0) row_ptr[static_cast<int64_t>(pt.num_q_heads) * M] = nnz;
   } else {
     base = wt.seg_base[h * pt.num_segments + s];
   }
 #pragma unroll
   for (int k = 0; k < kNb; ++k) {
-    e.pos[k] = k < nb ? base + local[r0 + k] : 0;
+    e.pos[k] = k < nb ? base + loc[k] : 0;
     if (k < nb && lane == 0) row_ptr[r0 + k] = e.pos[k];
   }
-  e.ps = wt.lu_off[u];
-  e.wt = &wt;
-  e.base = e.ps;
-  const int32_t nw = wt.lu_nwork[u], plen = wt.lu_len[u];  // pieces
-  e.w0 = wt.lu_work0[u];
-  e.whole = nw == 1;
-  e.m0 = m0;
-  e.nb = nb;
-  e.below = (1ull << lane) - 1ull;
-  const int mlast = m0 + nb - 1;
-  constexpr bool grouped = kGrouped;
-  if constexpr (!grouped) {
-    // T >= 64: the candidates are the prompt's tiles lo .. mlast in order
-    // (the earlier documents' pages, then this segment's tiles), 64 per
-    // round; each round's loads are issued one round ahead.
-    //   query unit: M-block m0 + k lists n when n <= m0 + k (Section 5.1);
-    //   document unit: every M-block lists the CA-marked pages of the earlier
-    //   documents, and row r = i + k its LA-marked tiles j < r and j == r.
-    const bool query = pt.seg_kind[s] == kQuery;
-    const int lo = pt.tile_lo[m0];
-    const int sd0 = pt.seg_tile0[s];
-    const int i = m0 - sd0;
-    const uint8_t* lav =
-        query ? la : la + pt.seg_la_off[s] + static_cast<int64_t>(h) * la_nbytes(pt.seg_pages[s]);
-    struct Cand {
-      int4 ti;
-      int32_t row0;
-      unsigned bits;  // the CA byte (earlier documents) or the LA bits per M-block
-    };
-    auto fetch = [&](int n) {
-      Cand c{make_int4(0, 0, -1, 0), 0, 0u};
-      if (n <= mlast) {
-        c.ti = pt.tile_info[n];
-        c.row0 = pages.table == nullptr ? c.ti.x : kv_row0(pt, pages, n);
-        if (!query) {
-          if (n < sd0) {
-            c.bits = ca[c.ti.z + static_cast<int64_t>(h) * (c.ti.w >> 3)];
+  if constexpr (!kGrouped) {
+    for (int t0 = 0; t0 < ncross;) {
+#pragma unroll
+      for (int q = 0; q < kCopy; ++q) {
+        if (t0 + 64 * q >= ncross) break;
+        e.copy_round(yc[q], yr[q], min(64, ncross - t0 - 64 * q), lane);
+      }
+      t0 += 64 * kCopy;
+      if (t0 < ncross) load_copy(t0);
+    }
+    for (int c0 = start;;) {
+      const int nr = min(kChunk, (mlast - c0) / 64 + 1);
+#pragma unroll
+      for (int c = 0; c < kChunk; ++c) {
+        if (c >= nr) break;
+        const int n = c0 + 64 * c + lane;
+        unsigned listed = 0u;
+        if (n <= mlast) {
+          if (query) {
+            listed = n < m0 ? all : (all & ~((1u << (n - m0)) - 1u));
+          } else if (n < sd0) {
+            listed = raw[c][0] != 0u ? all : 0u;
           } else {
             const int j = n - sd0;
 #pragma unroll
-            for (int k = 0; k < kNb; ++k) {
+            for (int k = 0; k < 2; ++k) {
               const int r = i + k;
-              if (k < nb && j < r) c.bits |= static_cast<unsigned>(get_bit(lav, r * (r + 1) / 2 + j)) << k;
+              if (k < nb && j < r) listed |= ((raw[c][k] >> (7 - ((r * (r + 1) / 2 + j) & 7))) & 1u) << k;
             }
+            if (j >= i && j < i + nb) listed |= 1u << (j - i);  // the diagonal tile
           }
         }
+        int32_t row0 = tl[c].x;
+        if (pages.table != nullptr)
+          row0 = (row0 < 0 ? 0 : (row0 >= pages.num_pages ? pages.num_pages - 1 : row0)) * pt.tile;
+        e.emit_at(listed, n, row0, tl[c].y);
       }
-      return c;
-    };
-    Cand cur = fetch(lo + lane);
-    for (int n0 = lo; n0 <= mlast; n0 += 64) {
-      const int n = n0 + lane;
-      const Cand nxt = fetch(n + 64);
-      unsigned listed = 0u;
-      if (n <= mlast) {
-        if (query) {
-          listed = n < m0 ? all : (all & ~((1u << (n - m0)) - 1u));
-        } else if (n < sd0) {
-          listed = (cur.bits >> (7 - (cur.ti.w & 7))) & 1u ? all : 0u;
-        } else {
-          listed = cur.bits;
-          const int j = n - sd0;
-          if (j >= i && j < i + nb) listed |= 1u << (j - i);  // the diagonal tile
-        }
-      }
-      e.emit_at(listed, n, cur.row0, cur.ti.y);
-      cur = nxt;
+      c0 += 64 * kChunk;
+      if (c0 > mlast) break;
+      load_walk(c0);
     }
   } else if (pt.seg_kind[s] == kQuery) {
     // the same, segment by segment so that tile groups stay within one call
@@ -738,11 +847,13 @@ hipError_t launch_decode(const PlanTables& pt, const WorkTables& wt, const uint8
     // one count block per head; the write pass adds the heads' totals and
     // writes row_ptr[Hq M]
     hipLaunchKernelGGL(decode_count_head, dim3(static_cast<unsigned>(pt.num_q_heads)), dim3(1024),
-                       0, stream, pt, wt, la, ca, counts);
+                       0, stream, pt, wt, la, ca, counts, pages);
   } else {
     // one count block per (head, segment); the last one scans the totals
-    // and writes row_ptr[Hq M]
+    // and writes row_ptr[Hq M].  No cross lists: the write pass walks every
+    // page.
     w2.head_tot = nullptr;
+    w2.cross_col = nullptr;
     const int64_t blocks = static_cast<int64_t>(pt.num_q_heads) * pt.num_segments;
     hipLaunchKernelGGL(decode_count, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, pt,
                        wt, la, ca, counts, row_ptr);

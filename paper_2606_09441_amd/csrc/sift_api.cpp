@@ -86,6 +86,7 @@ struct HostPlan {
   std::vector<int32_t> tile_info;  // int4 per tile (see PlanTables::tile_info)
   std::vector<int32_t> unit_head, unit_m0, unit_nb, step_off;  // list units
   std::vector<int32_t> lu_work0, lu_nwork, lu_len;
+  std::vector<sift::UnitRec> urec;  // list units by descending cost (the decode write order)
   std::vector<int32_t> wk_head, wk_m0, wk_nb, wk_off, wk_slot;        // work units
   std::vector<int32_t> splits;  // int4 records (see WorkTables)
   std::vector<sift::WorkRec> rec;     // work units in locality order
@@ -226,6 +227,13 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
         order.push_back(u);
         ++u;
       }
+  // The decode write walks each unit's candidate tiles (its cost) in one
+  // wavefront: longest first over all heads, so that no long unit starts
+  // late.
+  std::vector<int32_t> worder(U);
+  std::iota(worder.begin(), worder.end(), 0);
+  std::stable_sort(worder.begin(), worder.end(),
+                   [&](int32_t x, int32_t y) { return unit_cost[x] > unit_cost[y]; });
   // A unit's merged list is a subset of the tiles from the prompt's first
   // to its last M-block.
   hp.step_off.assign(U + 1, 0);
@@ -281,6 +289,26 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
     if (parts > 1) hp.part_slots += parts;
   }
   if (W > i32max / 2) return SIFT_E_CAPACITY;
+  hp.urec.assign(U, sift::UnitRec{});
+  for (int64_t q = 0; q < U; ++q) {
+    const int32_t uu = worder[q];
+    const int32_t m0 = hp.unit_m0[uu], sg = hp.tile_seg[m0];
+    sift::UnitRec& r = hp.urec[q];
+    r.head = hp.unit_head[uu];
+    r.m0 = m0;
+    r.nb = hp.unit_nb[uu];
+    r.seg = sg;
+    r.lo = hp.tile_lo[m0];
+    r.sd0 = hp.seg_tile0[sg];
+    r.pages = hp.seg_pages[sg];
+    r.la_off = hp.seg_la_off[sg];
+    r.step_off = hp.step_off[uu];
+    r.work0 = hp.lu_work0[uu];
+    r.nwork = hp.lu_nwork[uu];
+    r.plen = hp.lu_len[uu];
+    r.query = hp.seg_kind[sg] == sift::kQuery ? 1 : 0;
+    r.hrows = hp.tile_len[m0] > 64 ? 3 : 1;
+  }
   // Work-unit records in locality order (work unit w is record w); the
   // launch order is made on the device after each decode, from the step
   // counts.
@@ -448,6 +476,7 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   const size_t o_lw0 = put(blob, hp.lu_work0);
   const size_t o_lnw = put(blob, hp.lu_nwork);
   const size_t o_llen = put(blob, hp.lu_len);
+  const size_t o_urec = put(blob, hp.urec);
   const size_t o_rec = put(blob, hp.rec);  // step counts and first steps: written by decode
   const size_t o_launch = put(blob, hp.launch);  // written by the schedule pass
   const size_t o_splits = put(blob, hp.splits);
@@ -463,7 +492,12 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   const size_t o_counts = align(blob.size());
   const size_t o_segbase = align(o_counts + rows * 4);
   const size_t o_headtot = align(o_segbase + static_cast<int64_t>(hp.num_segments) * num_q_heads * 4);
-  const size_t o_rowptr = align(o_headtot + static_cast<int64_t>(num_q_heads) * 4);
+  const size_t o_camark = align(o_headtot + static_cast<int64_t>(num_q_heads) * 4);
+  const size_t o_segcross = align(o_camark + rows);
+  const size_t o_crosscol =
+      align(o_segcross + static_cast<int64_t>(hp.num_segments) * num_q_heads * 4);
+  const size_t o_crossrows = align(o_crosscol + rows * 4);
+  const size_t o_rowptr = align(o_crossrows + rows * 8);
   const size_t o_col = align(o_rowptr + (rows + 1) * 4);
   const int64_t W = static_cast<int64_t>(hp.wk_head.size());
   const size_t o_steps = align(o_col + std::max<int64_t>(cap, 1) * 4);
@@ -556,6 +590,7 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   plan->wt.lu_work0 = P(o_lw0);
   plan->wt.lu_nwork = P(o_lnw);
   plan->wt.lu_len = P(o_llen);
+  plan->wt.urec = reinterpret_cast<const sift::UnitRec*>(P(o_urec));
   plan->wt.steps = reinterpret_cast<int2*>(P(o_steps));
   plan->wt.sub = tile < 64 ? reinterpret_cast<uint32_t*>(P(o_sub)) : nullptr;
   plan->wt.splits = reinterpret_cast<const int4*>(P(o_splits));
@@ -567,6 +602,10 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   plan->wt.sched_done = plan->wt.redo + 4;
   plan->wt.seg_base = P(o_segbase);
   plan->wt.head_tot = P(o_headtot);
+  plan->wt.ca_mark = reinterpret_cast<uint8_t*>(P(o_camark));
+  plan->wt.seg_cross = P(o_segcross);
+  plan->wt.cross_col = P(o_crosscol);
+  plan->wt.cross_rows = reinterpret_cast<int2*>(P(o_crossrows));
   plan->wt.num_units = static_cast<int32_t>(U);
   plan->wt.num_work = static_cast<int32_t>(W);
   plan->wt.num_splits = static_cast<int32_t>(hp.splits.size() / 4);

@@ -118,6 +118,22 @@ static_assert(sizeof(WorkRec) == 64, "one record per 64 bytes");
 static_assert(offsetof(WorkRec, step_cnt) == 36, "the step count is word 9 (read as int4 2, .y)");
 static_assert(offsetof(WorkRec, rank) == 8, "the rank is word 2 (read as int4 0, .z)");
 
+// A list unit as the decode write pass reads it (one record, built with the
+// plan): the pass takes them in record order, longest candidate walk first.
+struct alignas(64) UnitRec {
+  int32_t head, m0, nb, seg;  // query head, first M-block, M-blocks, their segment
+  int32_t lo;                 // first tile of the prompt
+  int32_t sd0;                // first tile of the segment
+  int32_t pages;              // the segment's pages
+  int32_t la_off;             // its LA vectors' byte offset (head 0)
+  int32_t step_off;           // first step of the unit's merged list (lu_off)
+  int32_t work0, nwork, plen;  // its work units: nwork pieces of plen steps from work0
+  int32_t query;              // 1 for a query segment
+  int32_t hrows;              // T = 128: kernel blocks of the M-block (3 or 1)
+  int32_t pad[2];
+};
+static_assert(sizeof(UnitRec) == 64, "one record per 64 bytes");
+
 struct WorkTables {
   WorkRec* rec;               // [W] locality order (device memory)
   WorkRec* launch;            // [grid] launch order (device scratch, written by the schedule pass)
@@ -131,6 +147,7 @@ struct WorkTables {
   const int32_t* lu_work0;    // [U]
   const int32_t* lu_nwork;    // [U]
   const int32_t* lu_len;      // [U] piece length (a bound of the list when not split)
+  const UnitRec* urec;        // [U] the list units in decode write order
   int2* steps;                // [lu_off[U]] (device scratch)
   uint32_t* sub;              // [lu_off[U]] per step, T < 64 only: bit G k + s set when the
                               // unit's M-block k lists key tile s of the step (device scratch)
@@ -143,6 +160,14 @@ struct WorkTables {
   int32_t* decode_done;       // decode: finished count blocks (device scratch, zero between
                               // decodes)
   int32_t* head_tot;          // [Hq] decode: each query head's list entries (device scratch)
+  uint8_t* ca_mark;           // [Hq * M] decode: per (head, tile) 1 when a document tile's
+                              // page is CA-marked, else 0 (device scratch)
+  int32_t* seg_cross;         // [Hq * S] decode: CA-marked pages of the earlier documents
+                              // of each segment's prompt (device scratch)
+  int32_t* cross_col;         // [Hq * M] decode: per head, each prompt's CA-marked tiles in
+                              // tile order from its first tile's index on; nullptr when the
+                              // count pass does not build them (device scratch)
+  int2* cross_rows;           // [Hq * M] the same tiles' {first K/V row, length}
   int32_t* sched_done;        // [kNumXcd] schedule: finished blocks per chunk (device
                               // scratch, zero between decodes)
   int32_t* redo;              // [3] bf16 attention: {flag: do every unit again exactly,
@@ -190,7 +215,7 @@ struct TileSteps {
 
 __device__ __forceinline__ TileSteps tile_steps_at(const PlanTables& pt, int32_t n, unsigned listed,
                                                    int32_t m0, int32_t nb, int32_t row0,
-                                                   int32_t len) {
+                                                   int32_t len, unsigned rows) {
   TileSteps t;
   t.cnt = 0;
   if (listed == 0u) return t;
@@ -201,7 +226,6 @@ __device__ __forceinline__ TileSteps tile_steps_at(const PlanTables& pt, int32_t
                                  static_cast<int>(diag << kStepDiagShift));
     return t;
   }
-  const unsigned rows = pt.tile_len[m0] > 64 ? 3u : 1u;  // kernel blocks of the M-block
   const unsigned d0 = n == m0 ? 1u : 0u;
   t.cnt = len > 64 ? 2 : 1;
   t.s[0] = make_int2(row0, min(len, 64) | static_cast<int>(rows << kStepListedShift) |
@@ -217,7 +241,8 @@ __device__ __forceinline__ TileSteps tile_steps_at(const PlanTables& pt, int32_t
 __device__ __forceinline__ TileSteps tile_steps(const PlanTables& pt, const KvPages& pg, int32_t n,
                                                 unsigned listed, int32_t m0, int32_t nb) {
   if (listed == 0u) return TileSteps{0, {}};
-  return tile_steps_at(pt, n, listed, m0, nb, kv_row0(pt, pg, n), pt.tile_len[n]);
+  const unsigned rows = pt.tile_len[m0] > 64 ? 3u : 1u;  // kernel blocks of the M-block
+  return tile_steps_at(pt, n, listed, m0, nb, kv_row0(pt, pg, n), pt.tile_len[n], rows);
 }
 
 // Decode (Section 5.1): count, write, schedule.  The count pass writes each
