@@ -116,7 +116,8 @@ __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
 // Wavefronts 0-1 own the unit's first M-block, 2-3 its second.
 struct Step {
   unsigned sub;  // T < 64: the sub-tile mask of the step (bit G k + s: M-block k lists key tile s)
-  int tok0;  // first token of the key tile
+  int kvt;   // T < 64: this wavefront's K/V row base (see WorkTables::kvb)
+  int tok0;  // T >= 64: first token of the key tile; T < 64: the sub-tile mask
   int info;  // len | listed << 8 | diagonal << 12
   bool valid;
   __device__ __forceinline__ int len() const { return info & kStepLenMask; }
@@ -136,14 +137,17 @@ __device__ __forceinline__ Step make_step(int2 x, bool valid) {
   // for x would also wait for that step's DMA
   asm volatile("" : "+s"(s.tok0), "+s"(s.info));
   s.valid = valid;
+  s.sub = static_cast<unsigned>(s.tok0);
+  s.kvt = 0;  // set by the caller at T < 64
   if (!valid) s.info = kT;  // a full-length dummy for unconditional reloads
   return s;
 }
 
 // Buffer resource of one key tile of one kv head: base = its first row,
 // num_records = bytes through the last valid row (loads past it return 0).
-__device__ __forceinline__ i32x4 tile_rsrc(const __bf16* base, int len, int row_bytes) {
-  const unsigned long long a = reinterpret_cast<unsigned long long>(base);
+// At T < 64 the base is an address: a wavefront's rows may start further
+// into the step than into their own tile, so the base can precede the tensor.
+__device__ __forceinline__ i32x4 tile_rsrc(unsigned long long a, int len, int row_bytes) {
   const int valid = (len - 1) * row_bytes + kD * 2;
   return i32x4{static_cast<int>(static_cast<unsigned>(a)), static_cast<int>((a >> 32) & 0xffff),
                valid, kBufferWord3};

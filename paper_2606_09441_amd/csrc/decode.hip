@@ -316,6 +316,7 @@ struct Emitter {
   int32_t m0, nb;
   unsigned hrows;  // T = 128: kernel blocks of the M-block (tile_steps_at)
   unsigned long long below;
+  int32_t gt, grun;  // copy_gathered: entries done, first entry of the current run
 
   __device__ __forceinline__ void lists(unsigned listed, int32_t n) {
 #pragma unroll
@@ -396,6 +397,51 @@ struct Emitter {
     }
   }
 
+  // T < 64: one round of a document unit's earlier-document part from the
+  // head's cross list (n entries; the first cnt lanes hold entries gt ..,
+  // tile id c, {first row, length} r), listed by every M-block.  A step
+  // gathers G such tiles, adjacent or not, each wavefront of the kernel
+  // reading its rows from its own tile (kvb); a partial tile (the last of
+  // its document) ends its step, so that only a step's last tile is short.
+  // Entry t starts a step when (t - first entry of its run) % G == 0, runs
+  // ending after partial tiles.
+  __device__ __forceinline__ void copy_gathered(int32_t c, int2 r, int32_t cnt, int32_t n,
+                                                int lane) {
+    const int T = pt->tile, G = pt->group;
+    const bool valid = lane < cnt;
+#pragma unroll
+    for (int k = 0; k < kNb; ++k) {
+      if (k >= nb) break;
+      if (valid) col[pos[k] + lane] = c;
+      pos[k] += cnt;
+    }
+    const bool part = valid && r.y < T;
+    const unsigned long long pm = __ballot(part);
+    const unsigned long long pb = pm & below;
+    const int t = gt + lane;
+    const int run = pb != 0ull ? gt + (63 - __clzll(pb)) + 1 : grun;
+    const int q = (t - run) & (G - 1);
+    const unsigned long long sm = __ballot(valid && q == 0);
+    const int32_t idx = ps + __popcll(sm & (below | (1ull << lane))) - 1;
+    const int32_t kv = r.x - q * T;
+    int* kw = reinterpret_cast<int*>(wt->kvb);
+    if (valid) kw[4 * static_cast<int64_t>(idx) + q] = kv;
+    if (valid && (part || q == G - 1 || t == n - 1)) {
+      // the step's last tile: the step's record, and its unused kvb words
+      const unsigned lst = (2u << ((nb - 1) / G)) - 1u;
+      unsigned sub = 0u;
+      for (int k = 0; k < nb; ++k) sub |= ((2u << q) - 1u) << (G * k);
+      const int2 st = make_int2(static_cast<int>(sub),
+                                (q * T + r.y) | static_cast<int>(lst << kStepListedShift));
+      steps[idx] = st;
+      for (int x = q + 1; x < 4; ++x) kw[4 * static_cast<int64_t>(idx) + x] = kv;
+      if (whole && idx - base < kFirstSteps) wt->rec[w0].first[idx - base] = st;
+    }
+    ps += __popcll(sm);
+    if (pm != 0ull) grun = gt + (63 - __clzll(pm)) + 1;
+    gt += cnt;
+  }
+
   // T < 64.  The lanes hold tiles local = c0 + lane of one segment of P
   // tiles (c0 a multiple of 64, so a group never straddles two calls).  The
   // group's first lane gathers its members' bits and writes the step: the
@@ -434,11 +480,20 @@ struct Emitter {
       for (int b = 0; b < kUnitBlocks; ++b)
         if (n == m0 + G * b) diag |= 1u << b;
       const int32_t idx = ps + __popcll(mu & below);
-      const int2 st = make_int2(kv_row0(*pt, pages, n),
-                                len | static_cast<int>(lst << kStepListedShift) |
-                                    static_cast<int>(diag << kStepDiagShift));
+      const int32_t row0 = kv_row0(*pt, pages, n);
+      const int2 st = make_int2(static_cast<int>(sm), len | static_cast<int>(lst << kStepListedShift) |
+                                                      static_cast<int>(diag << kStepDiagShift));
       steps[idx] = st;
-      wt->sub[idx] = sm;
+      // the group's tiles are adjacent in the packed K/V; a page pool places
+      // each on its own
+      int4 kb = make_int4(row0, row0, row0, row0);
+      if (pages.table != nullptr) {
+        const int T = pt->tile;
+        if (cnt > 1) kb.y = kv_row0(*pt, pages, n + 1) - T;
+        if (cnt > 2) kb.z = kv_row0(*pt, pages, n + 2) - 2 * T;
+        if (cnt > 3) kb.w = kv_row0(*pt, pages, n + 3) - 3 * T;
+      }
+      wt->kvb[idx] = kb;
       if (whole && idx - base < kFirstSteps) wt->rec[w0].first[idx - base] = st;
     }
     ps += __popcll(mu);
@@ -485,7 +540,7 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   const uint8_t* lav = query ? la : la + ur.la_off + static_cast<int64_t>(h) * la_nbytes(ur.pages);
   const uint8_t* mark = wt.ca_mark + static_cast<int64_t>(h) * M;
   const int2* rowlen = reinterpret_cast<const int2*>(pt.tile_info);  // {first row, length} at 2 n
-  const bool copy = !kGrouped && !query && wt.cross_col != nullptr;
+  const bool copy = !query && wt.cross_col != nullptr;
   const int64_t ybase = static_cast<int64_t>(h) * M + lo;
   const int start = copy ? sd0 : lo;
   int32_t ncross = 0;
@@ -521,13 +576,11 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
       }
     }
   };
-  if constexpr (!kGrouped) {
-    if (copy) {
-      ncross = wt.seg_cross[h * pt.num_segments + s];
-      load_copy(0);
-    }
-    load_walk(start);
+  if (copy) {
+    ncross = wt.seg_cross[h * pt.num_segments + s];
+    load_copy(0);
   }
+  if constexpr (!kGrouped) load_walk(start);
   Emitter<kNb, kHalves> e;
   e.col = col;
   e.steps = wt.steps;
@@ -543,6 +596,7 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   e.nb = nb;
   e.hrows = static_cast<unsigned>(ur.hrows);
   e.below = (1ull << lane) - 1ull;
+  e.gt = e.grun = 0;
   int32_t base;
   if (wt.head_tot != nullptr) {
     // local[] holds offsets inside the head: add the totals of heads 0 .. h-1
@@ -622,14 +676,27 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
     }
   } else {
     // T < 64, a document unit.  CA pages of every earlier document: the
-    // same for all M-blocks
-    for (int d = pt.seg_first[s]; d < s; ++d) {
-      const int Pe = pt.seg_pages[d];
-      const uint8_t* cav = ca + pt.seg_ca_off[d] + static_cast<int64_t>(h) * ca_nbytes(Pe);
-      for (int c0 = 0; c0 < Pe; c0 += 64) {
-        const int b = c0 + lane;
-        const bool on = b < Pe && get_bit(cav, b);
-        e.emit_grouped(on ? all : 0u, pt.seg_tile0[d] + b, b, Pe, lane);
+    // same for all M-blocks; gathered G to a step from the cross list when
+    // the count pass built it
+    if (copy) {
+      for (int t0 = 0; t0 < ncross;) {
+#pragma unroll
+        for (int q = 0; q < kCopy; ++q) {
+          if (t0 + 64 * q >= ncross) break;
+          e.copy_gathered(yc[q], yr[q], min(64, ncross - t0 - 64 * q), ncross, lane);
+        }
+        t0 += 64 * kCopy;
+        if (t0 < ncross) load_copy(t0);
+      }
+    } else {
+      for (int d = pt.seg_first[s]; d < s; ++d) {
+        const int Pe = pt.seg_pages[d];
+        const uint8_t* cav = ca + pt.seg_ca_off[d] + static_cast<int64_t>(h) * ca_nbytes(Pe);
+        for (int c0 = 0; c0 < Pe; c0 += 64) {
+          const int b = c0 + lane;
+          const bool on = b < Pe && get_bit(cav, b);
+          e.emit_grouped(on ? all : 0u, pt.seg_tile0[d] + b, b, Pe, lane);
+        }
       }
     }
     // LA rows i .. i+nb-1 of the document's triangle, tiles j = 0 .. i+nb-1;
@@ -695,8 +762,11 @@ __global__ __launch_bounds__(256) void merge_steps(PlanTables pt, WorkTables wt,
   int pj = 0;                     // its place in that piece
   const int plen = wt.lu_len[u];  // piece length
   auto put = [&](int2 st, uint32_t sm) {
+    if (G > 1) {
+      wt.kvb[base + ns] = make_int4(st.x, st.x, st.x, st.x);  // adjacent tiles
+      st.x = static_cast<int>(sm);
+    }
     wt.steps[base + ns] = st;
-    if (G > 1) wt.sub[base + ns] = sm;
     if (pj < kFirstSteps) wt.rec[pw].first[pj] = st;
     if (++pj == plen) {  // the next step opens the next piece
       pj = 0;

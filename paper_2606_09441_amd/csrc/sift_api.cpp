@@ -505,10 +505,10 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   // (the lists' total length bound: one step per listed tile at T <= 64, up
   // to two at T = 128)
   const int64_t step_cap = hp.step_off.empty() ? 0 : hp.step_off.back();
-  const size_t o_sub = align(o_steps + (std::max<int64_t>(step_cap, 1) + 8) * 8);
-  // per-step sub-tile masks, T < 64 only
+  // per-step K/V row bases, T < 64 only
+  const size_t o_kvb = align(o_steps + (std::max<int64_t>(step_cap, 1) + 8) * 8);
   const size_t o_part_o =
-      align(o_sub + (tile < 64 ? (std::max<int64_t>(step_cap, 1) + 8) * 4 : 0));
+      align(o_kvb + (tile < 64 ? (std::max<int64_t>(step_cap, 1) + 8) * 16 : 0));
   const int64_t slot_rows = hp.part_slots * sift::kUnitRows;
   // the pieces' outputs: fp32, or bf16 plus the bf16 of its rounding error
   const size_t o_part_lo = align(o_part_o + slot_rows * head_dim * 4);
@@ -592,7 +592,7 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   plan->wt.lu_len = P(o_llen);
   plan->wt.urec = reinterpret_cast<const sift::UnitRec*>(P(o_urec));
   plan->wt.steps = reinterpret_cast<int2*>(P(o_steps));
-  plan->wt.sub = tile < 64 ? reinterpret_cast<uint32_t*>(P(o_sub)) : nullptr;
+  plan->wt.kvb = tile < 64 ? reinterpret_cast<int4*>(P(o_kvb)) : nullptr;
   plan->wt.splits = reinterpret_cast<const int4*>(P(o_splits));
   plan->wt.part_o = static_cast<void*>(P(o_part_o));
   plan->wt.part_lo = static_cast<void*>(P(o_part_lo));
@@ -874,8 +874,8 @@ sift_status sift_plan_run_paged(sift_plan* plan, const sift_tensor* q, const sif
   if (in.num_tiles > 0 && num_pages < 1) return SIFT_E_SHAPE;
   if (in.num_tiles > 0 && page_table == nullptr) return SIFT_E_NULL;
   if (q->dtype != k_pages->dtype || q->dtype != v_pages->dtype) return SIFT_E_UNSUPPORTED;
-  // bf16 pages of T < 64 rows: a 64-key step would span several pages
-  if (q->dtype == SIFT_BF16 && (in.tile < 64 || in.head_dim != 128)) return SIFT_E_UNSUPPORTED;
+  // bf16 at T < 64: a 64-key step's tiles each come from their own page
+  if (q->dtype == SIFT_BF16 && in.head_dim != 128) return SIFT_E_UNSUPPORTED;
   if (q->dtype == SIFT_F32 && (out->dtype != SIFT_F32 || in.tile > 64)) return SIFT_E_UNSUPPORTED;
   if (in.la_bytes > 0 && local_bitmap == nullptr) return SIFT_E_NULL;
   if (in.ca_bytes > 0 && cross_bitmap == nullptr) return SIFT_E_NULL;

@@ -53,11 +53,16 @@ __device__ __forceinline__ int32_t kv_row0(const PlanTables& pt, const KvPages& 
 
 // Attention work: a list unit = (query head, up to kUnitBlocks consecutive
 // M-blocks of one segment).  The decode pass writes each list unit's merged
-// step list (the union of its M-blocks' lists, in ascending key-tile order)
-// at steps[lu_off[u] ..]; lu_off[u+1] - lu_off[u] bounds its length.
+// step list (the union of its M-blocks' lists) at steps[lu_off[u] ..];
+// lu_off[u+1] - lu_off[u] bounds its length.
 // Step = {first K/V row of the key tile, len | listed << 8 | diagonal << 12},
 // where bit k of `listed` says M-block m0 + k lists the tile and bit k of
-// `diagonal` says the tile is m0 + k itself.
+// `diagonal` says the tile is m0 + k itself.  At T < 64 a step is 64 keys of
+// G = 64 / T tiles, bit b of `listed` / `diagonal` refers to kernel block b
+// (M-blocks G b ..), the first word is the sub-tile mask (bit G k + s: M-block
+// k lists the step's tile s) and kvb holds the tiles' K/V rows.  Steps run in
+// ascending key order, except that a document unit's steps over the earlier
+// documents gather G marked pages each, adjacent or not.
 //
 // A workgroup runs one work unit: a list unit's whole step list, or one piece
 // of it.  The query units, whose lists are long and of known length, are cut
@@ -149,8 +154,10 @@ struct WorkTables {
   const int32_t* lu_len;      // [U] piece length (a bound of the list when not split)
   const UnitRec* urec;        // [U] the list units in decode write order
   int2* steps;                // [lu_off[U]] (device scratch)
-  uint32_t* sub;              // [lu_off[U]] per step, T < 64 only: bit G k + s set when the
-                              // unit's M-block k lists key tile s of the step (device scratch)
+  int4* kvb;                  // [lu_off[U]] per step, T < 64 only: word q = the first K/V row
+                              // of the step's key sub-tile q minus q T (the step's 64 keys
+                              // are G tiles, not always adjacent ones; words past the
+                              // step's tiles repeat a valid one) (device scratch)
   const int4* splits;         // [NS] {record of the first piece, first slot, slots, 0}
   void* part_o;               // [slots][kUnitRows][head_dim], output type (device scratch)
   void* part_lo;              // bf16 output: the same shape, part_o's bf16 rounding error

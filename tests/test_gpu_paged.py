@@ -56,10 +56,13 @@ def _check(wl, tol, tag, full_oracle=True):
         dw.close()
 
 
-def test_paged_bf16_ragged_layouts():
-    wl = W.custom([[300, 64, 129, 75], [5], [1, 64, 0], [200, 131, 70]], tile=64, hq=8, hkv=2,
+@pytest.mark.parametrize("tile", [16, 32, 64])
+def test_paged_bf16_ragged_layouts(tile):
+    """At T < 64 a 64-key step holds 64 / T tiles, each read from its own
+    page."""
+    wl = W.custom([[300, 64, 129, 75], [5], [1, 64, 0], [200, 131, 70]], tile=tile, hq=8, hkv=2,
                   d=128, dtype="bf16", seed=7, p_la=0.4, p_ca=0.3)
-    _check(wl, BF16_TOL, "bf16 ragged layouts")
+    _check(wl, BF16_TOL, f"bf16 ragged layouts T={tile}")
 
 
 @pytest.mark.parametrize("tile,d", [(16, 64), (32, 128)])

@@ -1,10 +1,11 @@
 """GPU: bf16 attention at T = 16 and T = 32 (Section 4.3 takes T = 16 for
 storage).
 
-The bf16 kernel keeps 64-row blocks and 64-key steps: a step is a group of
-64 / T consecutive key tiles of one segment with a mask of which (row tile,
-key tile) pairs are listed.  Lists stay at T and are compared bit for bit;
-outputs against the fp64 oracle."""
+The bf16 kernel keeps 64-row blocks and 64-key steps: a step is 64 / T key
+tiles with a mask of which (row tile, key tile) pairs are listed, the tiles
+adjacent ones of one segment, or, over the earlier documents of a document's
+rows, any CA-marked pages (gathered).  Lists stay at T and are compared bit
+for bit; outputs against the fp64 oracle."""
 
 import numpy as np
 import pytest
@@ -76,22 +77,19 @@ def test_small_tile_split_query_units_sampled(tile):
 
 
 @pytest.mark.parametrize("tile", [16, 32])
-def test_small_tile_given_lists_and_paged_refusal(tile):
-    from paper_2606_09441_amd import SiftError
+def test_small_tile_given_lists(tile):
+    """Caller lists make steps of adjacent tiles only (no gathering): a
+    different grouping of the same keys, so compared with the oracle."""
     wl = _wl(tile, 41, 0.5, 0.4, hq=4)
     dw = DevWorkload(wl)
     try:
-        a = dw.run()
+        a = dw.run().float().cpu().numpy()
         rp, ci = dw.plan.decode(dw.la, dw.ca)
-        b = dw.plan.attention(dw.q, dw.k, dw.v, rp, ci)
-        torch.cuda.synchronize()
-        assert torch.equal(a, b), "given lists differ from decoded lists"
-        M = dw.plan.info["num_tiles"]
-        kp = torch.zeros((M * tile, wl.hkv, wl.d), dtype=dw.k.dtype, device=dw.k.device)
-        table = torch.arange(M, dtype=torch.int32, device=dw.k.device)
-        with pytest.raises(SiftError) as e:        # a 64-key step would span pages
-            dw.plan.run_paged(dw.q, kp, kp, table, dw.la, dw.ca)
-        assert e.value.status == 4
-        say(f"[tsmall] T={tile}: caller lists bit-identical, paged bf16 refused")
+        b = dw.plan.attention(dw.q, dw.k, dw.v, rp, ci).float().cpu().numpy()
     finally:
         dw.close()
+    ref = O.attention(oracle_layout(wl), wl.q, wl.k, wl.v, wl.la, wl.ca)
+    ea, eb = max_abs(a, ref), max_abs(b, ref)
+    say(f"[tsmall] T={tile}: decoded lists max-abs {ea:.3e}, caller lists {eb:.3e}")
+    assert np.isfinite(b).all()
+    assert ea <= BF16_TOL and eb <= BF16_TOL, (ea, eb)
