@@ -2,7 +2,7 @@
 
 The 64K layer (48/8 heads, D 128) with bits made at T = 16, 32 and 128 (the
 storage tile of Section 4.3 takes T = 16; Table 1's arithmetic implies
-T = 128), and the 16K layer (32/8 heads) at rho = 0.2 with T = 32.  Lists
+T = 128), and the 16K layer (32/8 heads) at rho = 0.2 with T = 32 and 16.  Lists
 are compared bit for bit; outputs on sampled rows of every head and on every
 query row of the first and last head, against the fp64 oracle."""
 
@@ -17,7 +17,7 @@ from oracle import sift_oracle as O
 pytestmark = pytest.mark.gpu
 
 CASES = [("long64k", {"tile": 16}), ("long64k", {"tile": 32}), ("long64k", {"tile": 128}),
-         ("llama8b_16k", {"rho": 0.2, "tile": 32})]
+         ("llama8b_16k", {"rho": 0.2, "tile": 32}), ("llama8b_16k", {"rho": 0.2, "tile": 16})]
 
 
 @pytest.mark.parametrize("name,kw", CASES, ids=[f"{n}-T{kw['tile']}" for n, kw in CASES])
