@@ -163,23 +163,20 @@ __global__ __launch_bounds__(1024) void decode_count_head(PlanTables pt, WorkTab
     if (m < M) {
       const int s = m0 == 0 ? seg0 : pt.tile_seg[m];
       const int i = m - pt.seg_tile0[s];
-      uint8_t mk = 0;
       if (pt.seg_kind[s] == kQuery) {
         cnt = m - pt.seg_tile0[first[s]] + 1;
       } else {
         const int P = pt.seg_pages[s];
         const uint8_t* lav = la + pt.seg_la_off[s] + static_cast<int64_t>(h) * la_nbytes(P);
         const uint8_t* cav = ca + pt.seg_ca_off[s] + static_cast<int64_t>(h) * ca_nbytes(P);
-        mk = static_cast<uint8_t>(get_bit(cav, i));
         const int32_t before = popc_bits(cav, 0, i);  // marked pages of s before i
         cnt = cross[s] + 1 + popc_bits(lav, i * (i + 1) / 2, i);
-        if (mk != 0) {
+        if (get_bit(cav, i)) {
           const int64_t y = static_cast<int64_t>(h) * M + pt.seg_tile0[first[s]] + cross[s] + before;
           wt.cross_col[y] = m;
           wt.cross_rows[y] = make_int2(kv_row0(pt, pages, m), pt.tile_len[m]);
         }
       }
-      wt.ca_mark[static_cast<int64_t>(h) * M + m] = mk;
     }
     int32_t incl;
     const int32_t chunk = block_scan1024(cnt, incl, wtot);

@@ -168,7 +168,8 @@ struct WorkTables {
                               // decodes)
   int32_t* head_tot;          // [Hq] decode: each query head's list entries (device scratch)
   uint8_t* ca_mark;           // [Hq * M] decode: per (head, tile) 1 when a document tile's
-                              // page is CA-marked, else 0 (device scratch)
+                              // page is CA-marked, else 0; written by the per-(head, segment)
+                              // count, whose write pass walks every page (device scratch)
   int32_t* seg_cross;         // [Hq * S] decode: CA-marked pages of the earlier documents
                               // of each segment's prompt (device scratch)
   int32_t* cross_col;         // [Hq * M] decode: per head, each prompt's CA-marked tiles in
@@ -252,10 +253,12 @@ __device__ __forceinline__ TileSteps tile_steps(const PlanTables& pt, const KvPa
   return tile_steps_at(pt, n, listed, m0, nb, kv_row0(pt, pg, n), pt.tile_len[n], rows);
 }
 
-// Decode (Section 5.1): count, write, schedule.  The count pass writes each
-// row's count as its offset inside its (head, segment) and scans the segment
-// totals; the write pass runs per unit, writes its rows' row_ptr, its
-// M-blocks' lists and the unit's merged step list.
+// Decode (Section 5.1): count, write, schedule.  The count pass gives each
+// row its offset inside its head and each head its total (or, for layouts of
+// more than 1024 segments, offsets inside and totals of each (head,
+// segment)), and the heads' cross lists; the write pass runs per unit,
+// writes its rows' row_ptr, its M-blocks' lists and the unit's merged step
+// list; the schedule pass orders the work units for the attention launch.
 hipError_t launch_decode(const PlanTables& pt, const WorkTables& wt, const uint8_t* la,
                          const uint8_t* ca, int32_t* counts, int32_t* row_ptr, int32_t* col_idx,
                          const KvPages& pages, hipStream_t stream);
