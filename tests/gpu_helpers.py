@@ -104,3 +104,24 @@ def workers() -> int:
     """Threads for the oracle: the host cores this process may use, at most 16."""
     import os
     return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def page_pool(wl, k, v, extra_pages=5, seed=0):
+    """Page pool [num_pages * T, Hkv, D] of a workload's K/V (device tensors
+    k, v) in a random page order, with NaN in the unused pages and page
+    tails, and its page table."""
+    import torch
+    lay = oracle_layout(wl)
+    M = lay.num_tiles
+    T = wl.tile
+    rng = np.random.default_rng(seed)
+    num_pages = M + extra_pages
+    perm = rng.permutation(num_pages)[:M].astype(np.int32)
+    kp = torch.full((num_pages * T, wl.hkv, wl.d), float("nan"), dtype=k.dtype, device=k.device)
+    vp = torch.full_like(kp, float("nan"))
+    for m in range(M):
+        _, _, a, cnt = lay.tile_span(m)
+        p = int(perm[m])
+        kp[p * T: p * T + cnt] = k[a: a + cnt]
+        vp[p * T: p * T + cnt] = v[a: a + cnt]
+    return kp, vp, torch.from_numpy(perm).to(k.device)

@@ -11,36 +11,19 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_helpers import BF16_TOL, F32_TOL, DevWorkload, max_abs, oracle_layout, say, workload
+from gpu_helpers import (BF16_TOL, F32_TOL, DevWorkload, max_abs, oracle_layout, page_pool, say,
+                         workload)
 from oracle import sift_oracle as O
 import workloads as W
 
 pytestmark = pytest.mark.gpu
 
 
-def _pool(wl, k, v, extra_pages=5, seed=0):
-    """Page pool [num_pages * T, Hkv, D] and page table of a workload."""
-    lay = oracle_layout(wl)
-    M = lay.num_tiles
-    T = wl.tile
-    rng = np.random.default_rng(seed)
-    num_pages = M + extra_pages
-    perm = rng.permutation(num_pages)[:M].astype(np.int32)
-    kp = torch.full((num_pages * T, wl.hkv, wl.d), float("nan"), dtype=k.dtype, device=k.device)
-    vp = torch.full_like(kp, float("nan"))
-    for m in range(M):
-        _, _, a, cnt = lay.tile_span(m)
-        p = int(perm[m])
-        kp[p * T: p * T + cnt] = k[a: a + cnt]
-        vp[p * T: p * T + cnt] = v[a: a + cnt]
-    return kp, vp, torch.from_numpy(perm).to(k.device)
-
-
 def _check(wl, tol, tag, full_oracle=True):
     dw = DevWorkload(wl)
     try:
         packed = dw.run()
-        kp, vp, table = _pool(wl, dw.k, dw.v)
+        kp, vp, table = page_pool(wl, dw.k, dw.v)
         paged = dw.plan.run_paged(dw.q, kp, vp, table, dw.la, dw.ca)
         torch.cuda.synchronize()
         assert torch.isfinite(paged.float()).all(), tag
@@ -81,7 +64,7 @@ def test_paged_argument_errors():
     wl = W.custom([[130, 64], [70, 20]], tile=64, hq=4, hkv=2, d=128, dtype="bf16", seed=3)
     dw = DevWorkload(wl)
     try:
-        kp, vp, table = _pool(wl, dw.k, dw.v)
+        kp, vp, table = page_pool(wl, dw.k, dw.v)
         with pytest.raises(SiftError) as e:   # not whole pages
             dw.plan.run_paged(dw.q, kp[:-1], vp[:-1], table, dw.la, dw.ca)
         assert e.value.status == 2
@@ -110,7 +93,7 @@ def test_paged_out_of_range_entries_stay_in_the_pool():
     wl = W.custom([[130, 64], [70, 20]], tile=64, hq=4, hkv=2, d=128, dtype="bf16", seed=4)
     dw = DevWorkload(wl)
     try:
-        kp, vp, table = _pool(wl, dw.k, dw.v, extra_pages=0)
+        kp, vp, table = page_pool(wl, dw.k, dw.v, extra_pages=0)
         kp = torch.nan_to_num(kp, nan=0.0)
         vp = torch.nan_to_num(vp, nan=0.0)
         bad = table.clone()

@@ -5,13 +5,14 @@ query of 0-100 tokens), a tile size, head counts and bit densities, then
 compares the decoded lists with the oracle's bit for bit and the outputs
 with the fp64 oracle.  Small layouts take the per-head count and the
 cross-list copy; the cases cover every tile size of the bf16 path (adjacent
-and gathered steps) and the fp32 path."""
+and gathered steps) and the fp32 path.  Some of them run again with K/V in a
+page pool, which must give the packed run's outputs bit for bit."""
 
 import numpy as np
 import pytest
 
-from gpu_helpers import (BF16_TOL, F32_TOL, DevWorkload, max_abs, oracle_csr, oracle_layout, say,
-                         workers)
+from gpu_helpers import (BF16_TOL, F32_TOL, DevWorkload, max_abs, oracle_csr, oracle_layout,
+                         page_pool, say, workers)
 from oracle import sift_oracle as O
 import workloads as W
 
@@ -54,3 +55,21 @@ def test_random_layout(seed):
     say(f"[rand] {tag}: lists bit-exact, max-abs {err:.3e}")
     assert np.isfinite(out).all(), tag
     assert err <= tol, (tag, err)
+
+
+@pytest.mark.parametrize("seed", range(0, 48, 3))
+def test_random_layout_paged(seed):
+    layout, kw = _case(seed)
+    wl = W.custom(layout, **kw)
+    dw = DevWorkload(wl)
+    try:
+        packed = dw.run()
+        kp, vp, table = page_pool(wl, dw.k, dw.v, seed=seed)
+        paged = dw.plan.run_paged(dw.q, kp, vp, table, dw.la, dw.ca)
+        import torch
+        torch.cuda.synchronize()
+        assert torch.isfinite(paged.float()).all()
+        assert torch.equal(packed, paged), f"seed {seed}: paged differs from packed"
+    finally:
+        dw.close()
+    say(f"[rand] seed {seed} T={kw['tile']} {kw['dtype']}: paged bit-identical to packed")
