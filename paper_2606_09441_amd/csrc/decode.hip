@@ -314,6 +314,19 @@ struct Emitter {
   unsigned hrows;  // T = 128: kernel blocks of the M-block (tile_steps_at)
   unsigned long long below;
   int32_t gt, grun;  // copy_gathered: entries done, first entry of the current run
+  int32_t nw, plen;  // the unit's pieces and their length (emit_grouped)
+
+  // A step's place among the first steps of its piece (read by the attention
+  // kernel's prologue from the work record).
+  __device__ __forceinline__ void note_first(int32_t idx, int2 st) {
+    const int32_t rel = idx - base;
+    if (whole) {
+      if (rel < kFirstSteps) wt->rec[w0].first[rel] = st;
+    } else {
+      const int32_t k = rel / plen, j = rel - k * plen;
+      if (j < kFirstSteps && k < nw) wt->rec[w0 + k].first[j] = st;
+    }
+  }
 
   __device__ __forceinline__ void lists(unsigned listed, int32_t n) {
 #pragma unroll
@@ -481,6 +494,7 @@ struct Emitter {
       const int2 st = make_int2(static_cast<int>(sm), len | static_cast<int>(lst << kStepListedShift) |
                                                       static_cast<int>(diag << kStepDiagShift));
       steps[idx] = st;
+      note_first(idx, st);
       // the group's tiles are adjacent in the packed K/V; a page pool places
       // each on its own
       int4 kb = make_int4(row0, row0, row0, row0);
@@ -491,7 +505,6 @@ struct Emitter {
         if (cnt > 3) kb.w = kv_row0(*pt, pages, n + 3) - 3 * T;
       }
       wt->kvb[idx] = kb;
-      if (whole && idx - base < kFirstSteps) wt->rec[w0].first[idx - base] = st;
     }
     ps += __popcll(mu);
   }
@@ -509,7 +522,7 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
                                                     int32_t* __restrict__ col, KvPages pages) {
   const int lane = threadIdx.x & 63;
   const int slot = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
-  if (slot >= wt.num_units) return;  // uniform per wavefront
+  if (slot >= wt.num_urec) return;  // uniform per wavefront
   const UnitRec ur = wt.urec[slot];
   const int h = ur.head, m0 = ur.m0, nb = ur.nb, s = ur.seg;
   const int M = pt.num_tiles;
@@ -532,7 +545,7 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   //   their results is used (raw bytes kept, bits taken later), so a chunk
   //   waits on memory once.
   constexpr int kChunk = 4, kCopy = 4;
-  const bool query = ur.query != 0;
+  const bool query = (ur.flags & kUnitQuery) != 0;
   const int lo = ur.lo, sd0 = ur.sd0, i = m0 - sd0;
   const uint8_t* lav = query ? la : la + ur.la_off + static_cast<int64_t>(h) * la_nbytes(ur.pages);
   const uint8_t* mark = wt.ca_mark + static_cast<int64_t>(h) * M;
@@ -584,14 +597,16 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   e.pt = &pt;
   e.wt = &wt;
   e.pages = pages;
-  e.ps = ur.step_off;
-  e.base = e.ps;
+  e.base = ur.step_off;
+  e.ps = e.base + ur.part_skip;
   const int32_t nw = ur.nwork, plen = ur.plen;  // pieces
   e.w0 = ur.work0;
   e.whole = nw == 1;
+  e.nw = nw;
+  e.plen = plen;
   e.m0 = m0;
   e.nb = nb;
-  e.hrows = static_cast<unsigned>(ur.hrows);
+  e.hrows = static_cast<unsigned>((ur.flags >> 1) & 3);
   e.below = (1ull << lane) - 1ull;
   e.gt = e.grun = 0;
   int32_t base;
@@ -613,10 +628,15 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
   } else {
     base = wt.seg_base[h * pt.num_segments + s];
   }
+  // a part of a query unit starts after the earlier segments' tiles, which
+  // every M-block lists
+  const int32_t skip = kGrouped && query ? pt.seg_tile0[ur.part_d0] - lo : 0;
+  const bool first_part = (ur.flags & kUnitFirstPart) != 0;
 #pragma unroll
   for (int k = 0; k < kNb; ++k) {
     e.pos[k] = k < nb ? base + loc[k] : 0;
-    if (k < nb && lane == 0) row_ptr[r0 + k] = e.pos[k];
+    if (k < nb && lane == 0 && first_part) row_ptr[r0 + k] = e.pos[k];
+    e.pos[k] += skip;
   }
   if constexpr (!kGrouped) {
     for (int t0 = 0; t0 < ncross;) {
@@ -659,9 +679,10 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
       if (c0 > mlast) break;
       load_walk(c0);
     }
-  } else if (pt.seg_kind[s] == kQuery) {
+  } else if (query) {
     // the same, segment by segment so that tile groups stay within one call
-    for (int d = pt.seg_first[s]; d <= s; ++d) {
+    // (this record's segments of the prompt)
+    for (int d = ur.part_d0; d < ur.part_d1; ++d) {
       const int last = d < s ? pt.seg_pages[d] - 1 : mlast - pt.seg_tile0[s];
       for (int c0 = 0; c0 <= last; c0 += 64) {
         const int j = c0 + lane;
@@ -713,7 +734,7 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
     }
   }
   const int32_t cnt = e.ps - e.base;
-  if (!e.whole) {
+  if (!kGrouped && !e.whole) {
     // the first steps of every piece, read back from the finished list (the
     // workgroup-scope fence waits for this wavefront's stores, which its
     // CU's loads then see)
@@ -723,7 +744,7 @@ __global__ __launch_bounds__(256) void decode_write(PlanTables pt, WorkTables wt
       if (k * plen + j < cnt) wt.rec[e.w0 + k].first[j] = wt.steps[e.base + k * plen + j];
     }
   }
-  write_work_counts(wt, e.w0, nw, plen, cnt, lane, 64);
+  if (ur.flags & kUnitLastPart) write_work_counts(wt, e.w0, nw, plen, cnt, lane, 64);
 }
 
 // Generic merge of caller-given lists (one thread per unit): the union of
@@ -928,7 +949,7 @@ hipError_t launch_decode(const PlanTables& pt, const WorkTables& wt, const uint8
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (wt.num_units == 0) return hipSuccess;
-  const dim3 wgrid(static_cast<unsigned>((wt.num_units + 3) / 4));
+  const dim3 wgrid(static_cast<unsigned>((wt.num_urec + 3) / 4));
   if (pt.group == 4)
     hipLaunchKernelGGL((decode_write<8, true, false>), wgrid, dim3(256), 0, stream, pt, w2, la, ca,
                        counts, row_ptr, col_idx, pages);

@@ -227,13 +227,6 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
         order.push_back(u);
         ++u;
       }
-  // The decode write walks each unit's candidate tiles (its cost) in one
-  // wavefront: longest first over all heads, so that no long unit starts
-  // late.
-  std::vector<int32_t> worder(U);
-  std::iota(worder.begin(), worder.end(), 0);
-  std::stable_sort(worder.begin(), worder.end(),
-                   [&](int32_t x, int32_t y) { return unit_cost[x] > unit_cost[y]; });
   // A unit's merged list is a subset of the tiles from the prompt's first
   // to its last M-block.
   hp.step_off.assign(U + 1, 0);
@@ -289,11 +282,17 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
     if (parts > 1) hp.part_slots += parts;
   }
   if (W > i32max / 2) return SIFT_E_CAPACITY;
-  hp.urec.assign(U, sift::UnitRec{});
-  for (int64_t q = 0; q < U; ++q) {
-    const int32_t uu = worder[q];
+  // Records of the decode write pass: one per unit, except that at T < 64 a
+  // query unit's walk (segment by segment over its prompt, in steps of G
+  // adjacent tiles) is cut into parts of whole segments of about kPartTiles
+  // tiles, one wavefront each.  They run longest walk first over all heads,
+  // so that no long walk starts late.
+  constexpr int64_t kPartTiles = 256;
+  std::vector<int64_t> rcost;
+  for (int64_t uu = 0; uu < U; ++uu) {
     const int32_t m0 = hp.unit_m0[uu], sg = hp.tile_seg[m0];
-    sift::UnitRec& r = hp.urec[q];
+    const bool query = hp.seg_kind[sg] == sift::kQuery;
+    sift::UnitRec r{};
     r.head = hp.unit_head[uu];
     r.m0 = m0;
     r.nb = hp.unit_nb[uu];
@@ -306,9 +305,49 @@ sift_status build_host_plan(const sift_layout* lay, int32_t hq, int32_t hkv, int
     r.work0 = hp.lu_work0[uu];
     r.nwork = hp.lu_nwork[uu];
     r.plen = hp.lu_len[uu];
-    r.query = hp.seg_kind[sg] == sift::kQuery ? 1 : 0;
-    r.hrows = hp.tile_len[m0] > 64 ? 3 : 1;
+    r.flags = (query ? sift::kUnitQuery : 0) | ((hp.tile_len[m0] > 64 ? 3 : 1) << 1);
+    r.part_d0 = hp.seg_first[sg];
+    r.part_d1 = sg + 1;
+    r.part_skip = 0;
+    if (!(query && G > 1)) {
+      r.flags |= sift::kUnitFirstPart | sift::kUnitLastPart;
+      hp.urec.push_back(r);
+      rcost.push_back(unit_cost[uu]);
+      continue;
+    }
+    // segment d's tiles walked by the unit, and its steps (groups of G)
+    const int32_t mlast = m0 + r.nb - 1;
+    auto tiles = [&](int32_t d) { return d < sg ? hp.seg_pages[d] : mlast - hp.seg_tile0[sg] + 1; };
+    int32_t skip = 0;
+    for (int32_t d0 = r.part_d0; d0 <= sg;) {
+      int32_t d1 = d0;
+      int64_t t = 0, g = 0;
+      while (d1 <= sg && (d1 == d0 || t + tiles(d1) <= kPartTiles)) {
+        t += tiles(d1);
+        g += (tiles(d1) + G - 1) / G;
+        ++d1;
+      }
+      sift::UnitRec p = r;
+      p.part_d0 = d0;
+      p.part_d1 = d1;
+      p.part_skip = skip;
+      if (d0 == r.part_d0) p.flags |= sift::kUnitFirstPart;
+      if (d1 == sg + 1) p.flags |= sift::kUnitLastPart;
+      hp.urec.push_back(p);
+      rcost.push_back(t);
+      skip += static_cast<int32_t>(g);
+      d0 = d1;
+    }
   }
+  {
+    std::vector<int32_t> ro(hp.urec.size());
+    std::iota(ro.begin(), ro.end(), 0);
+    std::stable_sort(ro.begin(), ro.end(), [&](int32_t x, int32_t y) { return rcost[x] > rcost[y]; });
+    std::vector<sift::UnitRec> sorted(hp.urec.size());
+    for (size_t q = 0; q < ro.size(); ++q) sorted[q] = hp.urec[ro[q]];
+    hp.urec.swap(sorted);
+  }
+  if (hp.urec.size() > static_cast<size_t>(i32max / 2)) return SIFT_E_CAPACITY;
   // Work-unit records in locality order (work unit w is record w); the
   // launch order is made on the device after each decode, from the step
   // counts.
@@ -607,6 +646,7 @@ sift_status create_plan(const sift_layout* layout, int32_t num_q_heads, int32_t 
   plan->wt.cross_col = P(o_crosscol);
   plan->wt.cross_rows = reinterpret_cast<int2*>(P(o_crossrows));
   plan->wt.num_units = static_cast<int32_t>(U);
+  plan->wt.num_urec = static_cast<int32_t>(hp.urec.size());
   plan->wt.num_work = static_cast<int32_t>(W);
   plan->wt.num_splits = static_cast<int32_t>(hp.splits.size() / 4);
   plan->wt.chunk_size = static_cast<int32_t>(hp.chunk_size);

@@ -123,8 +123,11 @@ static_assert(sizeof(WorkRec) == 64, "one record per 64 bytes");
 static_assert(offsetof(WorkRec, step_cnt) == 36, "the step count is word 9 (read as int4 2, .y)");
 static_assert(offsetof(WorkRec, rank) == 8, "the rank is word 2 (read as int4 0, .z)");
 
-// A list unit as the decode write pass reads it (one record, built with the
-// plan): the pass takes them in record order, longest candidate walk first.
+// A list unit, or a part of one, as the decode write pass reads it (one
+// record, built with the plan): the pass takes them in record order, longest
+// walk first.  At T < 64 a query unit's walk over its prompt is cut into
+// parts of whole segments: its lists are every tile of the prompt up to the
+// M-block, so where a part's entries and steps start is known in advance.
 struct alignas(64) UnitRec {
   int32_t head, m0, nb, seg;  // query head, first M-block, M-blocks, their segment
   int32_t lo;                 // first tile of the prompt
@@ -133,11 +136,15 @@ struct alignas(64) UnitRec {
   int32_t la_off;             // its LA vectors' byte offset (head 0)
   int32_t step_off;           // first step of the unit's merged list (lu_off)
   int32_t work0, nwork, plen;  // its work units: nwork pieces of plen steps from work0
-  int32_t query;              // 1 for a query segment
-  int32_t hrows;              // T = 128: kernel blocks of the M-block (3 or 1)
-  int32_t pad[2];
+  int32_t flags;              // kUnitQuery | hrows << 1 (T = 128: kernel blocks of the
+                              // M-block, 3 or 1) | kUnitFirstPart | kUnitLastPart
+  int32_t part_d0, part_d1;   // T < 64 query unit: the part's segments [d0, d1)
+  int32_t part_skip;          // steps of the unit before the part
 };
 static_assert(sizeof(UnitRec) == 64, "one record per 64 bytes");
+constexpr int32_t kUnitQuery = 1;
+constexpr int32_t kUnitFirstPart = 8;  // writes the rows' row_ptr
+constexpr int32_t kUnitLastPart = 16;  // writes the work units' step counts
 
 struct WorkTables {
   WorkRec* rec;               // [W] locality order (device memory)
@@ -183,6 +190,7 @@ struct WorkTables {
                               // launches), launches whose exact pass ran (a count kept
                               // for the plan's life)} (device scratch)
   int32_t num_units;          // U
+  int32_t num_urec;           // records of the decode write pass (units and parts)
   int32_t num_work;           // W
   int32_t num_splits;         // NS
   int32_t chunk_size;         // work units per XCD chunk
