@@ -127,19 +127,29 @@ __global__ __launch_bounds__(1024) void decode_count_head(PlanTables pt, WorkTab
                                                           KvPages pages) {
   __shared__ int32_t cross[kCountSegs];  // CA popcount, then the pages a row of s sees
   __shared__ int32_t first[kCountSegs];  // first segment of the prompt
+  __shared__ int32_t sgt[5][kCountSegs];  // first tile, pages, kind, LA and CA offsets
   __shared__ int32_t wtot[16];
   const int S = pt.num_segments;
   const int M = pt.num_tiles;
   const int h = blockIdx.x;
   const int t = threadIdx.x;
-  // the first rows' segments, issued early (independent of what follows)
-  int seg0 = t < M ? pt.tile_seg[t] : 0;
+  constexpr int kQ = 4;  // rows t + 1024 q of a group, their loads issued together
+  int sq[kQ];
+#pragma unroll
+  for (int q = 0; q < kQ; ++q) sq[q] = t + 1024 * q < M ? pt.tile_seg[t + 1024 * q] : 0;
   for (int s = t; s < S; s += 1024) {
     const int P = pt.seg_pages[s];
+    const int kind = pt.seg_kind[s];
+    const int caoff = pt.seg_ca_off[s];
     first[s] = pt.seg_first[s];
-    cross[s] = pt.seg_kind[s] == kQuery
+    sgt[0][s] = pt.seg_tile0[s];
+    sgt[1][s] = P;
+    sgt[2][s] = kind;
+    sgt[3][s] = pt.seg_la_off[s];
+    sgt[4][s] = caoff;
+    cross[s] = kind == kQuery
                    ? 0
-                   : popc_bits(ca + pt.seg_ca_off[s] + static_cast<int64_t>(h) * ca_nbytes(P), 0, P);
+                   : popc_bits(ca + caoff + static_cast<int64_t>(h) * ca_nbytes(P), 0, P);
   }
   __syncthreads();
   // per prompt, in segment order: each segment's rows see the pages its
@@ -157,31 +167,46 @@ __global__ __launch_bounds__(1024) void decode_count_head(PlanTables pt, WorkTab
   __syncthreads();
   int32_t* lrow = local + static_cast<int64_t>(h) * M;
   int32_t run = 0;
-  for (int m0 = 0; m0 < M; m0 += 1024) {
-    const int m = m0 + t;
-    int32_t cnt = 0;
-    if (m < M) {
-      const int s = m0 == 0 ? seg0 : pt.tile_seg[m];
-      const int i = m - pt.seg_tile0[s];
-      if (pt.seg_kind[s] == kQuery) {
-        cnt = m - pt.seg_tile0[first[s]] + 1;
-      } else {
-        const int P = pt.seg_pages[s];
-        const uint8_t* lav = la + pt.seg_la_off[s] + static_cast<int64_t>(h) * la_nbytes(P);
-        const uint8_t* cav = ca + pt.seg_ca_off[s] + static_cast<int64_t>(h) * ca_nbytes(P);
-        const int32_t before = popc_bits(cav, 0, i);  // marked pages of s before i
-        cnt = cross[s] + 1 + popc_bits(lav, i * (i + 1) / 2, i);
-        if (get_bit(cav, i)) {
-          const int64_t y = static_cast<int64_t>(h) * M + pt.seg_tile0[first[s]] + cross[s] + before;
-          wt.cross_col[y] = m;
-          wt.cross_rows[y] = make_int2(kv_row0(pt, pages, m), pt.tile_len[m]);
+  for (int g0 = 0; g0 < M; g0 += 1024 * kQ) {
+    if (g0 > 0) {
+#pragma unroll
+      for (int q = 0; q < kQ; ++q) {
+        const int m = g0 + 1024 * q + t;
+        sq[q] = m < M ? pt.tile_seg[m] : 0;
+      }
+    }
+    int32_t cnt[kQ];
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) {
+      const int m = g0 + 1024 * q + t;
+      cnt[q] = 0;
+      if (m < M) {
+        const int s = sq[q];
+        const int i = m - sgt[0][s];
+        if (sgt[2][s] == kQuery) {
+          cnt[q] = m - sgt[0][first[s]] + 1;
+        } else {
+          const int P = sgt[1][s];
+          const uint8_t* lav = la + sgt[3][s] + static_cast<int64_t>(h) * la_nbytes(P);
+          const uint8_t* cav = ca + sgt[4][s] + static_cast<int64_t>(h) * ca_nbytes(P);
+          const int32_t before = popc_bits(cav, 0, i);  // marked pages of s before i
+          cnt[q] = cross[s] + 1 + popc_bits(lav, i * (i + 1) / 2, i);
+          if (get_bit(cav, i)) {
+            const int64_t y = static_cast<int64_t>(h) * M + sgt[0][first[s]] + cross[s] + before;
+            wt.cross_col[y] = m;
+            wt.cross_rows[y] = make_int2(kv_row0(pt, pages, m), pt.tile_len[m]);
+          }
         }
       }
     }
-    int32_t incl;
-    const int32_t chunk = block_scan1024(cnt, incl, wtot);
-    if (m < M) lrow[m] = run + incl - cnt;
-    run += chunk;
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) {
+      if (g0 + 1024 * q >= M) break;  // uniform
+      int32_t incl;
+      const int32_t chunk = block_scan1024(cnt[q], incl, wtot);
+      if (g0 + 1024 * q + t < M) lrow[g0 + 1024 * q + t] = run + incl - cnt[q];
+      run += chunk;
+    }
   }
   if (t == 0) wt.head_tot[h] = run;
 }
