@@ -393,6 +393,45 @@ __device__ __forceinline__ void pv_tile(const PvArgs& v, int slot_off, const bf1
     for (int db = 0; db < 4; ++db) st.o[db] = mfma(v_frag(v, slot_off, db, s), pb[s], st.o[db]);
 }
 
+// QK^T of the next tile and the softmax weights of the current one, by hand:
+// k-step s issues its two MFMAs, the exponentials of four of the current
+// tile's sixteen score pairs, and the K fragment reads of k-step s + 2, then
+// a scheduling barrier keeps that order (two fragment pairs in flight).
+__device__ __forceinline__ void qk_exp_pipelined(const QkArgs& q, int slot_off,
+                                                 const bf16x8 (&qf)[8], f32x16& s0, f32x16& s1,
+                                                 const f32x16& c0, const f32x16& c1, float c,
+                                                 float base, bf16x8 (&pb)[4], float& lsum) {
+  const bf16x2 ones = bf16x2{static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
+  bf16x8 a0 = k_frag(q, slot_off, 0, 0), a1 = k_frag(q, slot_off, 1, 0);
+  bf16x8 b0 = k_frag(q, slot_off, 0, 1), b1 = k_frag(q, slot_off, 1, 1);
+  float psum = 0.f;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    s0 = mfma(a0, qf[s], s == 0 ? f32x16{} : s0);
+    s1 = mfma(a1, qf[s], s == 0 ? f32x16{} : s1);
+    const int st = s >> 1, e0 = (s & 1) * 4, v0 = 8 * (st & 1);
+#pragma unroll
+    for (int u = 0; u < 4; u += 2) {
+      const float x0 = (st < 2) ? c0[v0 + e0 + u] : c1[v0 + e0 + u];
+      const float x1 = (st < 2) ? c0[v0 + e0 + u + 1] : c1[v0 + e0 + u + 1];
+      const float p0 = __builtin_amdgcn_exp2f(fmaf(x0, c, -base));
+      const float p1 = __builtin_amdgcn_exp2f(fmaf(x1, c, -base));
+      const bf16x2 pp = bf16x2{static_cast<__bf16>(p0), static_cast<__bf16>(p1)};
+      pb[st][e0 + u] = pp[0];
+      pb[st][e0 + u + 1] = pp[1];
+      psum = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, psum, false);
+    }
+    a0 = b0;
+    a1 = b1;
+    if (s + 2 < 8) {
+      b0 = k_frag(q, slot_off, 0, s + 2);
+      b1 = k_frag(q, slot_off, 1, s + 2);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  lsum += psum;
+}
+
 // Interleave QK^T of the next tile (16 LDS reads, 16 MFMAs) with the
 // softmax exponentials of the current one, and PV of the current tile (32
 // transpose reads, 16 MFMAs) with the row max of the next one.
