@@ -395,8 +395,8 @@ __device__ __forceinline__ void pv_tile(const PvArgs& v, int slot_off, const bf1
 
 // QK^T of the next tile and the softmax weights of the current one, by hand:
 // k-step s issues its two MFMAs, the exponentials of four of the current
-// tile's sixteen score pairs, and the K fragment reads of k-step s + 2, then
-// a scheduling barrier keeps that order (two fragment pairs in flight).
+// tile's sixteen score pairs, and the K fragment reads of k-step s + 3, then
+// a scheduling barrier keeps that order (three fragment pairs in flight).
 __device__ __forceinline__ void qk_exp_pipelined(const QkArgs& q, int slot_off,
                                                  const bf16x8 (&qf)[8], f32x16& s0, f32x16& s1,
                                                  const f32x16& c0, const f32x16& c1, float c,
@@ -404,6 +404,7 @@ __device__ __forceinline__ void qk_exp_pipelined(const QkArgs& q, int slot_off,
   const bf16x2 ones = bf16x2{static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
   bf16x8 a0 = k_frag(q, slot_off, 0, 0), a1 = k_frag(q, slot_off, 1, 0);
   bf16x8 b0 = k_frag(q, slot_off, 0, 1), b1 = k_frag(q, slot_off, 1, 1);
+  bf16x8 d0 = k_frag(q, slot_off, 0, 2), d1 = k_frag(q, slot_off, 1, 2);
   float psum = 0.f;
 #pragma unroll
   for (int s = 0; s < 8; ++s) {
@@ -423,13 +424,37 @@ __device__ __forceinline__ void qk_exp_pipelined(const QkArgs& q, int slot_off,
     }
     a0 = b0;
     a1 = b1;
-    if (s + 2 < 8) {
-      b0 = k_frag(q, slot_off, 0, s + 2);
-      b1 = k_frag(q, slot_off, 1, s + 2);
+    b0 = d0;
+    b1 = d1;
+    if (s + 3 < 8) {
+      d0 = k_frag(q, slot_off, 0, s + 3);
+      d1 = k_frag(q, slot_off, 1, s + 3);
     }
     __builtin_amdgcn_sched_barrier(0);
   }
   lsum += psum;
+}
+
+// QK^T alone, the same way.
+__device__ __forceinline__ void qk_pipelined(const QkArgs& q, int slot_off, const bf16x8 (&qf)[8],
+                                             f32x16& s0, f32x16& s1) {
+  bf16x8 a0 = k_frag(q, slot_off, 0, 0), a1 = k_frag(q, slot_off, 1, 0);
+  bf16x8 b0 = k_frag(q, slot_off, 0, 1), b1 = k_frag(q, slot_off, 1, 1);
+  bf16x8 d0 = k_frag(q, slot_off, 0, 2), d1 = k_frag(q, slot_off, 1, 2);
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    s0 = mfma(a0, qf[s], s == 0 ? f32x16{} : s0);
+    s1 = mfma(a1, qf[s], s == 0 ? f32x16{} : s1);
+    a0 = b0;
+    a1 = b1;
+    b0 = d0;
+    b1 = d1;
+    if (s + 3 < 8) {
+      d0 = k_frag(q, slot_off, 0, s + 3);
+      d1 = k_frag(q, slot_off, 1, s + 3);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
 }
 
 // Interleave QK^T of the next tile (16 LDS reads, 16 MFMAs) with the
