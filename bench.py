@@ -199,6 +199,8 @@ def main():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-hh8", action="store_true",
                     help="skip the heavy-hitter x8 leg (long64k only)")
+    ap.add_argument("--no-low-toggle", action="store_true",
+                    help="skip timing the attention on mantissa-cleared inputs")
     ap.add_argument("--no-extract", action="store_true",
                     help="skip the offline metadata extraction leg")
     ap.add_argument("--only-extract", action="store_true",
@@ -382,6 +384,27 @@ def main():
         log(f"heavy-hitter x8: attention {ms_attn_h:.3f} ms, exact pass in {ran} of {n_h} launches")
         del kh, qh, vh, lah, cah, wh
 
+    low_toggle = None
+    if wl.dtype == "bf16" and not args.no_low_toggle:
+        # the same lists and instruction stream on inputs whose bits switch
+        # less: Q, K and V with their mantissas cleared (sign and exponent
+        # kept), timed in turn with the inputs themselves
+        clear = lambda x: (x.view(torch.int16) & -128).view(torch.bfloat16)
+        ql, kl, vl = clear(q), clear(k), clear(v)
+        plan.decode_internal(la, ca)
+        n_l = max(2, args.steps // 2)
+        ms_l, ms_r = [], []
+        for _ in range(2):
+            ms_l.append(per_launch(lambda: plan.attention_internal(ql, kl, vl, out=out), n_l))
+            ms_r.append(per_launch(lambda: plan.attention_internal(q, k, v, out=out), n_l))
+        low_toggle = {"attention_ms": round(float(np.mean(ms_l)), 4),
+                      "attention_ms_unmodified": round(float(np.mean(ms_r)), 4),
+                      "note": "Q, K, V with their bf16 mantissas cleared, same lists and "
+                              "launches, interleaved with the unmodified inputs: the speed "
+                              "depends on how many operand bits switch"}
+        log(f"mantissas cleared: attention {np.mean(ms_l):.3f} ms against {np.mean(ms_r):.3f} ms")
+        del ql, kl, vl
+
     one_shot = None
     if wl.dtype == "bf16":
         from paper_2606_09441_amd import sparse_prefill
@@ -485,6 +508,7 @@ def main():
         "exact_pass": exact,
         "heavy_hitters_x8": heavy,
         "one_shot": one_shot,
+        "low_toggle": low_toggle,
         "roofline": {
             "bound": "mfma",
             "achieved": round(achieved, 2),
